@@ -1,0 +1,22 @@
+"""Seeded synthetic workloads for the shallow-fusion decode step.
+
+This package only draws inputs: a Zipf token corpus, a Kneser-Ney n-gram
+language model estimated from it (the model is an *input* of the fusion step,
+exactly as a user-supplied ARPA file would be), phrase lists and joint logits.
+It holds none of the fusion arithmetic (no backoff evaluation, no trie, no
+scoring).  Both the CPU oracle and the GPU library read what it produces.
+"""
+
+from .gen import (  # noqa: F401
+    CONFIGS,
+    LMArrays,
+    Phrases,
+    Workload,
+    make_corpus,
+    estimate_kn,
+    make_phrases,
+    make_logits,
+    load_workload,
+    tiny_random_lm,
+    tiny_random_phrases,
+)
