@@ -1,0 +1,90 @@
+// Device images of the n-gram tables and the phrase tree, shared by the host
+// builders (ngram_tables.cpp, boost_trie.cpp) and the fusion kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+
+#include "fusion.h"
+
+namespace fusion {
+
+// ---------------------------------------------------------------------------
+// NgramTables
+//
+// Level L of a context means its last L tokens: c_1 = the last token, c_m =
+// the state itself (m <= N-1).  The LM row of a state sigma is resolved
+// bottom-up in the order the backoff recursion fixes:
+//   level 1    dense[c_1][y] = p*(c_1 y) if that bigram exists,
+//              else uni(y) + bo(c_1)                       (one fp32 add)
+//   level L>=2 the arcs of c_L (successors y with p*(c_L y)) override the
+//              row; every level above the one an entry came from adds its
+//              backoff in increasing L.
+// A state record inlines the chain c_2..c_m so that one load resolves it.
+// ---------------------------------------------------------------------------
+struct LMDevice {
+  const float *dense = nullptr;        // [(V+2) * V]  level-1 row of every one-token context
+  const int32_t *dense_next = nullptr; // [(V+2) * V]  state after y when the winner is level <= 1
+  const int32_t *cnt1 = nullptr;       // [V+2]        explicit bigram successors with y < V
+  const int32_t *rec = nullptr;        // [(n_states - (V+2)) * rec_stride] state records
+  const int2 *arcs[FUSION_MAX_ORDER] = {};  // arcs[L], L = 2..N-1: (token, logp bits) of order L+1
+  const int32_t *top_next = nullptr;   // [n_N]  state after an order-N arc
+  int64_t off[FUSION_MAX_ORDER + 2] = {};   // off[k] = first id of order-k states (k >= 2)
+  int64_t n_states = 0;
+  int32_t N = 0, V = 0, blank = 0, rec_stride = 0, eos_ok = 0, pad = 0;
+};
+
+// record of a state of order m >= 2 (int32 words):
+//   [0]                     c_1 | (m << 16)
+//   [1 + 3*(L-2) + 0]       bo(c_L) as float bits      (L = 2..m)
+//   [1 + 3*(L-2) + 1]       first arc of c_L in arcs[L]
+//   [1 + 3*(L-2) + 2]       number of arcs of c_L
+inline int record_stride(int N) {
+  int w = 1 + 3 * (N > 2 ? N - 2 : 0);
+  return (w + 3) & ~3;  // 16-byte records
+}
+
+// ---------------------------------------------------------------------------
+// BoostTrie
+//
+// The phrase automaton with its failure links compiled out: the root keeps a
+// dense row (target node and entry value E per token); every other node q
+// keeps the sorted list of tokens whose transition differs from the root's
+// (its own children, then those inherited along its failure chain).
+//   node[q]  = (phi(q) bits, first delta entry, delta count, depth)
+//   delta[i] = (token, target node, E(target) bits, 0)
+// boost(y|q) = E(target) - phi(q).
+// ---------------------------------------------------------------------------
+struct TrieDevice {
+  const int4 *node = nullptr;
+  const int4 *delta = nullptr;
+  const int32_t *root_target = nullptr;  // [V]
+  const float *root_E = nullptr;         // [V]
+  int32_t n_nodes = 0, V = 0, blank = 0, max_depth = 0;
+};
+
+}  // namespace fusion
+
+struct NgramTables {
+  fusion::LMDevice dev;
+  int64_t n[FUSION_MAX_ORDER + 1] = {};
+  int64_t device_bytes = 0;
+  void *allocs[16] = {};
+  int n_allocs = 0;
+};
+
+struct BoostTrie {
+  fusion::TrieDevice dev;
+  int64_t n_delta = 0;
+  int64_t device_bytes = 0;
+  void *allocs[8] = {};
+  int n_allocs = 0;
+};
+
+namespace fusion {
+// thread-local error text behind fusion_last_error()
+int set_error(int code, const std::string &msg);
+int hip_error(hipError_t e, const char *what);
+}  // namespace fusion
