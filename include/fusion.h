@@ -73,7 +73,8 @@ enum {
 };
 
 /* status bits reported by fusion_device_status */
-enum { FUSION_STATUS_BAD_LM_STATE = 1, FUSION_STATUS_BAD_BOOST_STATE = 2 };
+enum { FUSION_STATUS_BAD_LM_STATE = 1, FUSION_STATUS_BAD_BOOST_STATE = 2,
+       FUSION_STATUS_SYNC_TIMEOUT = 4 /* a beam stream's workgroups failed to meet (results invalid) */ };
 
 /* limits of this build */
 #define FUSION_MAX_ORDER 8   /* n-gram order N */

@@ -147,7 +147,7 @@ extern "C" int boost_build(int32_t vocab, int32_t blank_id, int32_t n_phrases, c
   for (int32_t q = 0; q < n; ++q) {
     int32_t pb;
     std::memcpy(&pb, &phi[q], 4);
-    node[q] = make_int4(pb, (int32_t)dl.size(), (int32_t)delta[q].size(), depth[q]);
+    node[q] = make_int4(pb, (int32_t)dl.size(), (int32_t)delta[q].size(), q);
     for (auto &yt : delta[q]) {
       int32_t eb;
       std::memcpy(&eb, &E[yt.second], 4);
@@ -155,10 +155,10 @@ extern "C" int boost_build(int32_t vocab, int32_t blank_id, int32_t n_phrases, c
     }
   }
   if (dl.size() > (size_t)INT32_MAX) return set_error(FUSION_E_UNSUPPORTED, "boost_build: transition lists too large");
-  std::vector<int32_t> root_target(V, 0);
-  std::vector<float> root_E(V, 0.0f);
+  std::vector<int4> root_node(V, node[0]);
+  std::vector<float> root_E(V, E[0]);
   for (auto &yc : kids[0]) {
-    root_target[yc.first] = yc.second;
+    root_node[yc.first] = node[yc.second];
     root_E[yc.first] = E[yc.second];
   }
   auto *t = new BoostTrie();
@@ -183,7 +183,7 @@ extern "C" int boost_build(int32_t vocab, int32_t blank_id, int32_t n_phrases, c
   };
   int rc = put(node.data(), node.size() * sizeof(int4), (const void **)&t->dev.node);
   if (rc == FUSION_OK) rc = put(dl.data(), dl.size() * sizeof(int4), (const void **)&t->dev.delta);
-  if (rc == FUSION_OK) rc = put(root_target.data(), root_target.size() * 4, (const void **)&t->dev.root_target);
+  if (rc == FUSION_OK) rc = put(root_node.data(), root_node.size() * sizeof(int4), (const void **)&t->dev.root_node);
   if (rc == FUSION_OK) rc = put(root_E.data(), root_E.size() * 4, (const void **)&t->dev.root_E);
   if (rc == FUSION_OK) {
     hipError_t e = hipStreamSynchronize(stream);

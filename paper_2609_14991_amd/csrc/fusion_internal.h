@@ -23,10 +23,14 @@ namespace fusion {
 //              row; every level above the one an entry came from adds its
 //              backoff in increasing L.
 // A state record inlines the chain c_2..c_m so that one load resolves it.
+// The state reached from one-token context w by token y, when no context of
+// two or more tokens has an arc for y, is the bigram (w y) if it exists, else
+// the unigram (y); its record is stored again at rec_dense[w * V + y] so a
+// kernel reaches it from (w, y) with a single load.
 // ---------------------------------------------------------------------------
 struct LMDevice {
   const float *dense = nullptr;        // [(V+2) * V]  level-1 row of every one-token context
-  const int32_t *dense_next = nullptr; // [(V+2) * V]  state after y when the winner is level <= 1
+  const int32_t *rec_dense = nullptr;  // [(V+2) * V * rec_stride]  record of the state after (w, y)
   const int32_t *cnt1 = nullptr;       // [V+2]        explicit bigram successors with y < V
   const int32_t *rec = nullptr;        // [(n_states - (V+2)) * rec_stride] state records
   const int2 *arcs[FUSION_MAX_ORDER] = {};  // arcs[L], L = 2..N-1: (token, logp bits) of order L+1
@@ -36,13 +40,15 @@ struct LMDevice {
   int32_t N = 0, V = 0, blank = 0, rec_stride = 0, eos_ok = 0, pad = 0;
 };
 
-// record of a state of order m >= 2 (int32 words):
+// record of a state of order m (int32 words):
 //   [0]                     c_1 | (m << 16)
-//   [1 + 3*(L-2) + 0]       bo(c_L) as float bits      (L = 2..m)
-//   [1 + 3*(L-2) + 1]       first arc of c_L in arcs[L]
-//   [1 + 3*(L-2) + 2]       number of arcs of c_L
+//   [1]                     state id
+//   [2 + 3*(L-2) + 0]       bo(c_L) as float bits      (L = 2..m)
+//   [2 + 3*(L-2) + 1]       first arc of c_L in arcs[L]
+//   [2 + 3*(L-2) + 2]       number of arcs of c_L
+// (a one-token state w has m = 1 and no level entries)
 inline int record_stride(int N) {
-  int w = 1 + 3 * (N > 2 ? N - 2 : 0);
+  int w = 2 + 3 * (N > 2 ? N - 2 : 0);
   return (w + 3) & ~3;  // 16-byte records
 }
 
@@ -53,14 +59,15 @@ inline int record_stride(int N) {
 // dense row (target node and entry value E per token); every other node q
 // keeps the sorted list of tokens whose transition differs from the root's
 // (its own children, then those inherited along its failure chain).
-//   node[q]  = (phi(q) bits, first delta entry, delta count, depth)
 //   delta[i] = (token, target node, E(target) bits, 0)
 // boost(y|q) = E(target) - phi(q).
+//   node[q]      = (phi(q) bits, first delta entry, delta count, q)
+//   root_node[y] = node[root target of y]   (the state after y from the root)
 // ---------------------------------------------------------------------------
 struct TrieDevice {
   const int4 *node = nullptr;
   const int4 *delta = nullptr;
-  const int32_t *root_target = nullptr;  // [V]
+  const int4 *root_node = nullptr;       // [V]
   const float *root_E = nullptr;         // [V]
   int32_t n_nodes = 0, V = 0, blank = 0, max_depth = 0;
 };

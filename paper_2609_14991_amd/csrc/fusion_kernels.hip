@@ -1,28 +1,34 @@
 // Fusion step kernels for gfx950 and the C ABI entry points fusion_step /
-// fusion_run (Eq. (1) of the paper, Sec. III-C, with greedy or top-k
-// selection and a frame-synchronous beam).
+// fusion_run: Eq. (1) of the paper (Sec. III-C) with greedy or top-k
+// selection and a frame-synchronous beam.
 //
-// Work mapping.  A workgroup owns one stream; each hypothesis of the stream
-// is processed by a slot of 4 wavefronts (256 lanes).  Lane g of a slot owns
-// the tokens y = (c * 256 + g) * 4 + j (j < 4, c < NC), so every logits /
-// dense-row read is a coalesced 16-byte-per-lane strip, and the owned
-// values stay in registers for the whole step.  Up to 4 slots run side by
-// side (1024 lanes), so a beam of 4 is one workgroup.
+// Work mapping.  One workgroup per hypothesis (W = 64, 256 or 1024 lanes),
+// so a 64 x 4 beam keeps all 256 CUs busy.  Lane g owns the tokens
+// y = (c * W + g) * 4 + j (j < 4, c < NC): every logits row read is a
+// coalesced 16-byte strip per lane held in registers; the level-1 dense LM row
+// goes straight from HBM into the workgroup's LDS row (global_load_lds), where
+// the arcs of the longer contexts are then scattered.
 //
-// Per hypothesis and frame (all steps below are the method's, in order):
-//   1  row statistics (online max / sum-exp, raw argmax) from the logits;
-//   2  LM context chain from one state record (backoffs and arc ranges of
-//      every level), the level-1 dense row of the last token;
-//   3  LDS scatter of the explicit arcs of levels 2..m, level by level, each
-//      already summed with the backoffs above its level (the addition order
-//      of the backoff recursion), and of the phrase transitions of the state;
-//   4  key = (x + lambda*lm) + beta*boost per owned token, top-k per lane,
-//      top-k per wave by shuffles, top-k of the slot from the 4 wave lists;
-//   5  next LM / phrase state of each candidate from the winning entry;
-//   6  beam: per stream the best B of B*k candidates by fp64 running score.
-// No MFMA: this is a gather/scan with ~10 flops per score, bound by memory.
+// Per frame and hypothesis, the method's steps in order:
+//   1  one load brings the state record (the whole backoff chain: backoffs and
+//      arc ranges of every context level) and the phrase node; the logits row
+//      and the dense row are issued alongside;
+//   2  one load brings the arcs of all levels (flattened) and the phrase
+//      transitions of the state; meanwhile the row statistics are reduced
+//      (online max / sum-exp, raw argmax);
+//   3  the arcs are scattered into LDS level by level, each summed with the
+//      backoffs above its level (the addition order of the backoff
+//      recursion), and the phrase transitions with their entry values;
+//   4  key = (x + lambda*lm) + beta*boost per owned token, top-k per lane, per
+//      wave (shuffles) and per hypothesis; each candidate carries where its
+//      next LM / phrase state comes from, so no further lookup is needed;
+//   5  beam: the B workgroups of a stream publish their candidates, meet at a
+//      per-stream counter, and each ranks all B*k candidates (fp64 running
+//      score) to take its own new hypothesis.
+// No MFMA: ~10 flops per score over gathered data.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 #include <cmath>
 #include <cstring>
@@ -46,12 +52,12 @@ int hip_error(hipError_t e, const char *what) {
 
 namespace {
 
-constexpr int kSlotLanes = 256;
-constexpr int kWavesPerSlot = 4;
-constexpr int kMaxSlots = 4;
-constexpr int kMaxWaves = kMaxSlots * kWavesPerSlot;
-constexpr int kMaxB = FUSION_MAX_BEAM;
-constexpr int kMaxLevels = FUSION_MAX_ORDER;  // levels 2..N-1 < 8
+constexpr int kMaxWaves = 16;
+constexpr int kMaxLevels = FUSION_MAX_ORDER;  // context levels 1..N-1 <= 7
+constexpr int kAux = 256;                     // LDS side tables: phrase transitions, top-level next states
+constexpr int kNodeLane = 32;                 // lanes 32..35 of the record word hold the phrase node
+constexpr int kCounterStride = 16;            // ints between per-stream counters (one 64-byte line)
+constexpr int kSpinLimit = 1 << 20;           // bounded wait at the beam rendezvous (~1 s)
 
 __device__ int g_status;
 
@@ -66,197 +72,338 @@ struct Params {
   int32_t *parents;
   float *fused;
   int64_t *traffic;
-  float *scores;       // fusion_step outputs [H, k]
+  float *scores;  // fusion_step outputs [H, k]
   int32_t *next_lm;
   int32_t *next_boost;
-  int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, Vp, slots, pad;
+  int4 *xchg;     // beam exchange [S][2][B][k] candidate records of two int4
+  int *counters;  // [S * kCounterStride]
+  int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, pad;
   float lam, beta;
 };
 
 __device__ __forceinline__ bool before(float ka, int ya, float kb, int yb) {
   return ka > kb || (ka == kb && ya < yb);
 }
-
 __device__ __forceinline__ float as_float(int v) { return __int_as_float(v); }
-
+__device__ __forceinline__ int as_int(float v) { return __float_as_int(v); }
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int rdl(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 __device__ __forceinline__ unsigned long long umin64(unsigned long long a, unsigned long long b) {
   return a < b ? a : b;
 }
 
+// raw buffer access to one V-wide row: a 4-SGPR descriptor and a per-lane
+// byte offset; reads past the row return 0
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+__device__ __forceinline__ rsrc_t row_rsrc(const float *base, int n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), (short)0, n * 4, 0x00020000);
+}
+__device__ __forceinline__ float4 row_load4(rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ float row_load1(rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+__device__ __forceinline__ void row_store4(rsrc_t r, float4 v, int voff, int soff) {
+  typedef int v4i __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4i, v), r, voff, soff, 0);
+}
+__device__ __forceinline__ void row_store1(rsrc_t r, float v, int voff, int soff) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, voff, soff, 0);
+}
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+
+// record words: [0] c_1 | m << 16, [1] state id, [2 + 3(L-2) + {0,1,2}] = (bo, first arc, arcs) of level L
+__device__ __forceinline__ int rec_bo_lane(int L) { return 2 + 3 * (L - 2); }
+__device__ __forceinline__ int rec_beg_lane(int L) { return 3 + 3 * (L - 2); }
+__device__ __forceinline__ int rec_cnt_lane(int L) { return 4 + 3 * (L - 2); }
+
+// sorted per-lane candidate list: key desc, id asc; each entry carries where
+// the state after that token comes from (LM: state id, or -1 = the record at
+// (c_1, y); phrases: node id, or -1 = the root transition of y)
 template <int KM>
-__device__ __forceinline__ void topk_insert(float (&lk)[KM], int (&ly)[KM], float key, int y) {
-  if (!before(key, y, lk[KM - 1], ly[KM - 1])) return;
-  lk[KM - 1] = key;
-  ly[KM - 1] = y;
+struct TopK {
+  float k[KM];
+  int y[KM], lm[KM], q[KM];
+  __device__ __forceinline__ void init() {
 #pragma unroll
-  for (int i = KM - 1; i > 0; --i) {
-    if (before(lk[i], ly[i], lk[i - 1], ly[i - 1])) {
-      float tk = lk[i];
-      lk[i] = lk[i - 1];
-      lk[i - 1] = tk;
-      int ty = ly[i];
-      ly[i] = ly[i - 1];
-      ly[i - 1] = ty;
+    for (int i = 0; i < KM; ++i) {
+      k[i] = -INFINITY;
+      y[i] = INT_MAX;
+      lm[i] = 0;
+      q[i] = 0;
     }
   }
-}
+  __device__ __forceinline__ bool wants(float key, int yy) const { return before(key, yy, k[KM - 1], y[KM - 1]); }
+  __device__ __forceinline__ void insert(float key, int yy, int l, int qq) {
+    k[KM - 1] = key;
+    y[KM - 1] = yy;
+    lm[KM - 1] = l;
+    q[KM - 1] = qq;
+#pragma unroll
+    for (int i = KM - 1; i > 0; --i) {
+      if (before(k[i], y[i], k[i - 1], y[i - 1])) {
+        float tk = k[i]; k[i] = k[i - 1]; k[i - 1] = tk;
+        int ty = y[i]; y[i] = y[i - 1]; y[i - 1] = ty;
+        int tl = lm[i]; lm[i] = lm[i - 1]; lm[i - 1] = tl;
+        int tq = q[i]; q[i] = q[i - 1]; q[i - 1] = tq;
+      }
+    }
+  }
+  __device__ __forceinline__ void pop() {
+#pragma unroll
+    for (int i = 0; i < KM - 1; ++i) {
+      k[i] = k[i + 1];
+      y[i] = y[i + 1];
+      lm[i] = lm[i + 1];
+      q[i] = q[i + 1];
+    }
+    k[KM - 1] = -INFINITY;
+    y[KM - 1] = INT_MAX;
+  }
+};
 
-template <int NC, int KM, bool AL>
-__global__ void __launch_bounds__(NC >= 8 ? 512 : 1024) fusion_kernel(Params p) {
+// hypothesis state carried between frames (LDS, written by one lane)
+struct HypState {
+  int lmsrc, qsrc, y, c1p;  // where the state comes from (see TopK), token, parent's c_1
+  int c1, fl;               // last token of the LM context (-1: from the record); 1 alive, 2 invalid
+  int cur_lm, cur_q;        // ids of the state scored this frame
+  double S;                 // running beam score
+};
+
+template <int W, int NC, int KM, bool AL>
+__global__ void __launch_bounds__(W) fusion_kernel(Params p) {
+  constexpr int NW = W / 64;
+  constexpr int Vp = NC * 4 * W;
+  constexpr int kUA = W >= 1024 ? 1 : 4;  // arcs per lane fetched in the second hop
+  constexpr int kUD = W >= 1024 ? 1 : 2;  // phrase transitions per lane fetched in the second hop
   extern __shared__ __align__(16) unsigned char dyn[];
+  float *lmval = reinterpret_cast<float *>(dyn);
+  uint32_t *win = reinterpret_cast<uint32_t *>(dyn) + Vp;
+  uint16_t *win16 = reinterpret_cast<uint16_t *>(win);
+  float *sE = reinterpret_cast<float *>(dyn) + 2 * Vp;
+  int *sDT = reinterpret_cast<int *>(sE + kAux);
+  int *sTN = sDT + kAux;
   __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves], s_pax[kMaxWaves];
   __shared__ int s_paid[kMaxWaves];
-  __shared__ float s_wk[kMaxWaves][KM];
-  __shared__ int s_wy[kMaxWaves][KM];
-  __shared__ float s_cf[kMaxB][KM];
-  __shared__ int s_cy[kMaxB][KM], s_cl[kMaxB][KM], s_cq[kMaxB][KM], s_cn[kMaxB];
-  __shared__ int s_lm[kMaxB], s_q[kMaxB], s_c1[kMaxB];
-  __shared__ double s_sc[kMaxB];
-  __shared__ int n_lm[kMaxB], n_q[kMaxB], n_c1[kMaxB];
-  __shared__ double n_sc[kMaxB];
+  __shared__ float w_key[kMaxWaves][KM], w_fus[kMaxWaves][KM];
+  __shared__ int w_y[kMaxWaves][KM], w_lm[kMaxWaves][KM], w_q[kMaxWaves][KM];
+  __shared__ HypState hs;
+  __shared__ const int2 *s_arcs[kMaxLevels];
+  __shared__ long long s_sbase[kMaxLevels];
+  __shared__ int s_lbeg[kMaxLevels];  // first arc of each level of the current state
+  __shared__ int s_cfg[2];  // V, blank: re-read each frame so per-token masks stay inside the loop
   __shared__ unsigned long long s_bytes, s_steps;
-  __shared__ const int2 *s_arcs[kMaxLevels];  // arcs of level L
-  __shared__ long long s_sbase[kMaxLevels];   // state id of the first arc of level L (< 0: top level)
 
   const LMDevice &lm = p.lm;
   const TrieDevice &tr = p.tr;
-  const int tid = threadIdx.x;
-  const int slot = tid >> 8;
-  const int g = tid & (kSlotLanes - 1);
-  const int wave = tid >> 6;
-  const int lane = tid & 63;
-  const int wslot = (tid >> 6) & (kWavesPerSlot - 1);
-  const int B = p.B, V = p.V, blank = p.blank, K = p.k;
-  const int s = blockIdx.x;
-  const int H = p.S * B;
+  const int g = threadIdx.x;
+  const int wave = g >> 6;
+  const int lane = g & 63;
+  const int B = p.B, K = p.k;
   const int N = lm.N;
-  float *lmval = reinterpret_cast<float *>(dyn) + (size_t)slot * p.Vp;
-  uint32_t *win = reinterpret_cast<uint32_t *>(reinterpret_cast<float *>(dyn) + (size_t)p.slots * p.Vp) +
-                  (size_t)slot * p.Vp;
-  uint16_t *win16 = reinterpret_cast<uint16_t *>(win);
-  float *rootE = reinterpret_cast<float *>(dyn) + (size_t)2 * p.slots * p.Vp;  // shared by the slots
-
-  // ---- initial states --------------------------------------------------------
-  if (tid < B) {
-    const int h = s * B + tid;
-    int sig = p.lm_state[h];
-    s_lm[tid] = sig;
-    s_q[tid] = p.has_trie ? p.boost_state[h] : 0;
-    s_sc[tid] = (B > 1) ? p.hyp_score[h] : 0.0;
-    int c1 = -1;
-    if (sig >= 0 && sig < lm.n_states) c1 = sig < V + 2 ? sig : (lm.rec[(int64_t)(sig - V - 2) * lm.rec_stride] & 0xFFFF);
-    s_c1[tid] = c1;
+  const int RS = lm.rec_stride;
+  // workgroup -> (stream, hypothesis); with xcd_map the B workgroups of a stream
+  // share blockIdx mod 8, i.e. one XCD and its L2, for the per-frame exchange
+  int sl, b;
+  {
+    const int x = blockIdx.x;
+    if (p.xcd_map) {
+      const int r = x >> 3;
+      sl = (x & 7) + 8 * (r / B);
+      b = r % B;
+    } else {
+      sl = x / B;
+      b = x % B;
+    }
   }
-  if (tid == 0) {
+  const int s = sl + p.s_off;
+  const int H = p.S * B;
+  const int h = s * B + b;
+
+  // ---- prologue ------------------------------------------------------------------
+  if (g < kMaxLevels) {
+    s_arcs[g] = lm.arcs[g];
+    s_sbase[g] = (g >= 2 && g + 1 <= N - 1) ? lm.off[g + 1] : -1;
+  }
+  if (g == 0) {
+    s_cfg[0] = p.V;
+    s_cfg[1] = p.blank;
     s_bytes = 0;
     s_steps = 0;
+    const int V = p.V, blank = p.blank;
+    const int sig = p.lm_state[h];
+    const int q = p.has_trie ? p.boost_state[h] : 0;
+    const double sc = B > 1 ? p.hyp_score[h] : 0.0;
+    const bool ok_lm = sig >= 0 && sig < lm.n_states && sig != blank && (sig != V + 1 || lm.eos_ok);
+    const bool ok_q = !p.has_trie || (q >= 0 && q < tr.n_nodes);
+    const bool alive = B == 1 || sc > -INFINITY;
+    hs.lmsrc = sig;
+    hs.qsrc = q;
+    hs.y = -1;
+    hs.c1p = -1;
+    hs.c1 = (ok_lm && sig < V + 2) ? sig : -1;
+    hs.fl = (alive ? 1 : 0) | ((ok_lm && ok_q) ? 0 : 2);
+    hs.cur_lm = sig;
+    hs.cur_q = q;
+    hs.S = sc;
+    if (alive && !(ok_lm && ok_q))
+      atomicOr(&g_status, (ok_lm ? 0 : FUSION_STATUS_BAD_LM_STATE) | (ok_q ? 0 : FUSION_STATUS_BAD_BOOST_STATE));
   }
-  if (tid < kMaxLevels) {
-    s_arcs[tid] = lm.arcs[tid];
-    s_sbase[tid] = (tid >= 2 && tid + 1 <= N - 1) ? lm.off[tid + 1] : -1;
+  float rE[NC][4];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int y0 = (c * W + g) * 4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rE[c][j] = (p.has_trie && y0 + j < p.V) ? tr.root_E[y0 + j] : 0.0f;
+    *reinterpret_cast<uint4 *>(win + y0) = make_uint4(0u, 0u, 0u, 0u);
   }
-  // phrase entry values of the root row (state independent), one copy per workgroup
-  for (int y = tid; y < p.Vp; y += blockDim.x) rootE[y] = (p.has_trie && y < V) ? tr.root_E[y] : 0.0f;
   __syncthreads();
 
+  bool aborted = false;  // after one failed rendezvous this workgroup stops waiting
   for (int t = 0; t < p.T; ++t) {
-    for (int b0 = 0; b0 < B; b0 += p.slots) {
-      const int b = b0 + slot;
-      const bool act = b < B && (B == 1 || s_sc[b] > -INFINITY);
-      const int sig = act ? __builtin_amdgcn_readfirstlane(s_lm[b]) : 0;
-      const int q = act ? __builtin_amdgcn_readfirstlane(s_q[b]) : 0;
-      const int c1 = act ? __builtin_amdgcn_readfirstlane(s_c1[b]) : 0;
-      const bool ok_lm = act && sig >= 0 && sig < lm.n_states && sig != blank && (sig != V + 1 || lm.eos_ok) && c1 >= 0;
-      const bool ok_q = !p.has_trie || (q >= 0 && q < tr.n_nodes);
-      const bool ok = ok_lm && ok_q;
-      // ---- state record: backoff chain of the context ---------------------
-      int m = 1;
-      float bo[kMaxLevels];
-      int beg[kMaxLevels], cnt[kMaxLevels];
-#pragma unroll
-      for (int L = 0; L < kMaxLevels; ++L) {
-        bo[L] = 0.0f;
-        beg[L] = 0;
-        cnt[L] = 0;
-      }
-      if (ok && sig >= V + 2) {
-        const int32_t *r = lm.rec + (int64_t)(sig - V - 2) * lm.rec_stride;
-        m = __builtin_amdgcn_readfirstlane(r[0] >> 16);
-#pragma unroll
-        for (int L = 2; L < kMaxLevels; ++L)
-          if (L <= m) {
-            bo[L] = as_float(__builtin_amdgcn_readfirstlane(r[1 + 3 * (L - 2)]));
-            beg[L] = __builtin_amdgcn_readfirstlane(r[2 + 3 * (L - 2)]);
-            cnt[L] = __builtin_amdgcn_readfirstlane(r[3 + 3 * (L - 2)]);
-          }
-      }
-      float phiq = 0.0f;
-      int dbeg = 0, dcnt = 0;
-      if (ok && p.has_trie) {
-        int4 nd = tr.node[q];
-        phiq = as_float(__builtin_amdgcn_readfirstlane(nd.x));
-        dbeg = __builtin_amdgcn_readfirstlane(nd.y);
-        dcnt = __builtin_amdgcn_readfirstlane(nd.z);
-      }
-      // ---- logits row and level-1 dense row --------------------------------
-      const int64_t rowoff = ((int64_t)t * H + (int64_t)s * B + b) * V;
-      const float *xrow = p.logits + rowoff;
-      const float *drow = lm.dense + (int64_t)(c1 < 0 ? 0 : c1) * V;
-      float xv[NC][4], dv[NC][4];
+    const int V = uni(s_cfg[0]), blank = uni(s_cfg[1]);
+    const int fl = uni(hs.fl);
+    const bool act = (fl & 1) != 0;
+    const bool inv = act && (fl & 2) != 0;
+    const bool ok = act && !inv;
+    const int lmsrc = uni(hs.lmsrc), qsrc = uni(hs.qsrc), yin = uni(hs.y);
+    int c1 = uni(hs.c1);
+    // ---- hop 1: state record, phrase node, logits row ------------------------------
+    const int32_t *rp = nullptr;
+    if (ok) {
+      if (lmsrc < 0) rp = lm.rec_dense + ((int64_t)uni(hs.c1p) * V + yin) * RS;
+      else if (lmsrc >= V + 2) rp = lm.rec + (int64_t)(lmsrc - V - 2) * RS;
+    }
+    const int4 *np = nullptr;
+    if (ok && p.has_trie) np = qsrc < 0 ? tr.root_node + yin : tr.node + qsrc;
+    int rw = 0;  // lanes 0..RS-1: record words; lanes 32..35: phrase node
+    if (rp && lane < RS) rw = rp[lane];
+    if (np && lane >= kNodeLane && lane < kNodeLane + 4) rw = reinterpret_cast<const int *>(np)[lane - kNodeLane];
+    const int64_t rowoff = ((int64_t)t * H + h) * V;
+    const int voff = g * 16;
+    float xv[NC][4];
+    {
+      const rsrc_t xr = row_rsrc(p.logits + rowoff, act ? V : 0);
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
-        const int y0 = (c * kSlotLanes + g) * 4;
+        const int y0 = (c * W + g) * 4;
         if (AL) {
-          float4 xx = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-          float4 dd = make_float4(0.f, 0.f, 0.f, 0.f);
-          if (act && y0 < V) xx = *reinterpret_cast<const float4 *>(xrow + y0);
-          if (ok && y0 < V) dd = *reinterpret_cast<const float4 *>(drow + y0);
+          const float4 xx = row_load4(xr, voff, c * W * 16);
           xv[c][0] = xx.x; xv[c][1] = xx.y; xv[c][2] = xx.z; xv[c][3] = xx.w;
-          dv[c][0] = dd.x; dv[c][1] = dd.y; dv[c][2] = dd.z; dv[c][3] = dd.w;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) xv[c][j] = row_load1(xr, voff + 4 * j, c * W * 16);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (!act || y0 + j >= V) xv[c][j] = -INFINITY;
+      }
+    }
+    // the initial state of a run may need its record to learn c_1
+    if (ok && c1 < 0) c1 = rp ? (rdl(rw, 0) & 0xFFFF) : lmsrc;
+    // level-1 dense row straight into the LDS LM row; arcs scattered later overwrite it
+    if (ok) {
+      const float *drow = lm.dense + (int64_t)c1 * V;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int wbase = c * W + wave * 64;  // first 4-token strip of this wave
+        if (AL) {
+          const int y0 = (wbase + lane) * 4;
+          __builtin_amdgcn_global_load_lds(drow + (y0 < V ? y0 : 0), (lds_ptr_t)(lmval + wbase * 4), 16, 0, 0);
         } else {
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            xv[c][j] = (act && y0 + j < V) ? xrow[y0 + j] : -INFINITY;
-            dv[c][j] = (ok && y0 + j < V) ? drow[y0 + j] : 0.0f;
+            const int y = wbase * 4 + j * 64 + lane;
+            __builtin_amdgcn_global_load_lds(drow + (y < V ? y : 0), (lds_ptr_t)(lmval + wbase * 4 + j * 64), 4, 0, 0);
           }
         }
-        *reinterpret_cast<uint4 *>(win + y0) = make_uint4(0u, 0u, 0u, 0u);
       }
-      // ---- row statistics: online max / sum-exp and raw argmax --------------
-      float lmx = -INFINITY;
-      float ax = -INFINITY;
+    }
+    // ---- decode the record ------------------------------------------------------
+    const int m = rp ? (rdl(rw, 0) >> 16) : 1;
+    const int sid = rp ? rdl(rw, 1) : lmsrc;
+    const bool has_node = np != nullptr;
+    const float phiq = has_node ? as_float(rdl(rw, kNodeLane)) : 0.0f;
+    const int dbeg = has_node ? rdl(rw, kNodeLane + 1) : 0;
+    const int dcnt = has_node ? rdl(rw, kNodeLane + 2) : 0;
+    const int qid = has_node ? rdl(rw, kNodeLane + 3) : qsrc;
+    // backoffs of levels 2..7, +0.0 above m (an exact no-op on the sums)
+    float bo[kMaxLevels];
+#pragma unroll
+    for (int L = 2; L < kMaxLevels; ++L) bo[L] = (L <= m) ? as_float(rdl(rw, rec_bo_lane(L))) : 0.0f;
+    // ---- hop 2: first arcs of levels 2..m (flattened) and first phrase transitions --
+    int total_arcs = 0;
+    for (int L = 2; L <= m; ++L) total_arcs += rdl(rw, rec_cnt_lane(L));
+    if (!ok) total_arcs = 0;
+    // per-level counts and first arcs as uniform values (readlane at fixed
+    // lanes is valid whatever the active mask)
+    int lcnt[kMaxLevels], lbeg[kMaxLevels];
+#pragma unroll
+    for (int L = 2; L < kMaxLevels; ++L) {
+      lcnt[L] = (L <= m) ? rdl(rw, rec_cnt_lane(L)) : 0;
+      lbeg[L] = (L <= m) ? rdl(rw, rec_beg_lane(L)) : 0;
+    }
+    int2 ab[kUA];
+    int at[kUA], tn[kUA];  // at = level << 16 | offset within the level
+#pragma unroll
+    for (int u = 0; u < kUA; ++u) {
+      int f = u * W + g;
+      ab[u] = make_int2(INT_MAX, 0);
+      at[u] = 0;
+      tn[u] = 0;
+      // the level of flattened arc f: subtract the counts of the levels below
+      int L = 2, bL = lbeg[2];
+#pragma unroll
+      for (int L2 = 2; L2 < kMaxLevels - 1; ++L2) {
+        const bool past = (L == L2) && (f >= lcnt[L2]) && (L2 < m);
+        f = past ? f - lcnt[L2] : f;
+        L = past ? L2 + 1 : L;
+        bL = past ? lbeg[L2 + 1] : bL;
+      }
+      if (u * W + g < total_arcs) {
+        at[u] = (L << 16) | f;
+        ab[u] = s_arcs[L][bL + f];
+        if (L == N - 1 && f < kAux) tn[u] = lm.top_next[bL + f];
+      }
+    }
+    int4 dd[kUD];
+#pragma unroll
+    for (int u = 0; u < kUD; ++u) {
+      const int j = u * W + g;
+      dd[u] = make_int4(INT_MAX, 0, 0, 0);
+      if (j < dcnt) dd[u] = tr.delta[dbeg + j];
+    }
+    // ---- row statistics: online max / sum-exp and raw argmax --------------------
+    {
+      float lmx = -INFINITY, ax = -INFINITY, lsum = 0.0f;
       int aid = INT_MAX;
 #pragma unroll
       for (int c = 0; c < NC; ++c)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int y = (c * kSlotLanes + g) * 4 + j;
+          const int y = (c * W + g) * 4 + j;
           const float x = xv[c][j];
-          if (y < V) {
-            lmx = fmaxf(lmx, x);
-            if (x > ax) {
-              ax = x;
-              aid = y;
-            }
+          lmx = fmaxf(lmx, x);
+          if (x > ax) {
+            ax = x;
+            aid = y;
           }
         }
-      float lsum = 0.0f;
 #pragma unroll
       for (int c = 0; c < NC; ++c)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int y = (c * kSlotLanes + g) * 4 + j;
-          if (y < V && lmx > -INFINITY) lsum += expf(xv[c][j] - lmx);
-        }
+        for (int j = 0; j < 4; ++j)
+          if (xv[c][j] > -INFINITY) lsum += expf(xv[c][j] - lmx);
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
-        float om = __shfl_xor(lmx, off);
-        float os = __shfl_xor(lsum, off);
-        float oax = __shfl_xor(ax, off);
-        int oaid = __shfl_xor(aid, off);
-        float nm = fmaxf(lmx, om);
-        float a = (lmx > -INFINITY) ? lsum * expf(lmx - nm) : 0.0f;
-        float bb = (om > -INFINITY) ? os * expf(om - nm) : 0.0f;
+        const float om = __shfl_xor(lmx, off);
+        const float os = __shfl_xor(lsum, off);
+        const float oax = __shfl_xor(ax, off);
+        const int oaid = __shfl_xor(aid, off);
+        const float nm = fmaxf(lmx, om);
+        const float a = (lmx > -INFINITY) ? lsum * expf(lmx - nm) : 0.0f;
+        const float bb = (om > -INFINITY) ? os * expf(om - nm) : 0.0f;
         lmx = nm;
         lsum = a + bb;
         if (oax > ax || (oax == ax && oaid < aid)) {
@@ -270,307 +417,421 @@ __global__ void __launch_bounds__(NC >= 8 ? 512 : 1024) fusion_kernel(Params p) 
         s_pax[wave] = ax;
         s_paid[wave] = aid;
       }
-      __syncthreads();
-      // ---- scatter: phrase transitions, then LM arcs level by level ---------
-      if (ok && p.has_trie) {
-        for (int j = g; j < dcnt; j += kSlotLanes) {
-          const int y = tr.delta[dbeg + j].x;
-          win16[2 * y + 1] = (uint16_t)(j + 1);
-        }
+    }
+    if (ok && g == 0) {
+      hs.cur_lm = sid;
+      hs.cur_q = qid;
+      hs.c1 = c1;
+#pragma unroll
+      for (int L = 2; L < kMaxLevels; ++L) s_lbeg[L] = lbeg[L];
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the dense row has landed in LDS
+    __syncthreads();
+    // ---- scatter ------------------------------------------------------------------
+    // an arc of level L is stored summed with the backoffs of levels L+1.., the
+    // addition order of the backoff recursion
+    auto put_arc = [&](int L, int j, int2 a, int tnext) {
+      const int y = a.x;
+      if (y < V) {
+        float v = as_float(a.y);
+#pragma unroll
+        for (int L2 = 3; L2 < kMaxLevels; ++L2)
+          if (L2 > L) v = v + bo[L2];
+        lmval[y] = v;
+        win16[2 * y] = (uint16_t)((L << 13) | j);
+        if (L == N - 1 && j < kAux) sTN[j] = tnext;
       }
-      const int nphase = N - 2 > 1 ? N - 2 : 1;
-      for (int ph = 0; ph < nphase; ++ph) {
-        const int L = ph + 2;
-        if (ok && L <= m) {
-          int bL = 0, cL = 0;
+    };
+    if (ok) {
 #pragma unroll
-          for (int L2 = 2; L2 < kMaxLevels; ++L2)
-            if (L2 == L) {
-              bL = beg[L2];
-              cL = cnt[L2];
-            }
-          const int2 *A = s_arcs[L] + bL;
-          for (int j = g; j < cL; j += kSlotLanes) {
-            const int2 a = A[j];
-            const int y = a.x;
-            if (y < V) {
-              float v = as_float(a.y);
-#pragma unroll
-              for (int L2 = 3; L2 < kMaxLevels; ++L2)
-                if (L2 > L && L2 <= m) v = v + bo[L2];
-              lmval[y] = v;
-              win16[2 * y] = (uint16_t)((L << 13) | j);
-            }
-          }
-        }
-        __syncthreads();
-      }
-      // ---- keys, fused row, per-lane top-k ------------------------------------
-      float M = -INFINITY;
-      float amx = -INFINITY;
-      int am = INT_MAX;
-#pragma unroll
-      for (int w = 0; w < kWavesPerSlot; ++w) M = fmaxf(M, s_pm[slot * kWavesPerSlot + w]);
-      float Ssum = 0.0f;
-#pragma unroll
-      for (int w = 0; w < kWavesPerSlot; ++w) {
-        const int i = slot * kWavesPerSlot + w;
-        if (s_pm[i] > -INFINITY) Ssum += s_ps[i] * expf(s_pm[i] - M);
-        if (s_pax[i] > amx || (s_pax[i] == amx && s_paid[i] < am)) {
-          amx = s_pax[i];
-          am = s_paid[i];
-        }
-      }
-      const float lse = M + logf(Ssum);
-      const bool blank_by_am = (p.mode == FUSION_BLANK_AM) && am == blank;
-      float lk[KM];
-      int ly[KM];
-#pragma unroll
-      for (int i = 0; i < KM; ++i) {
-        lk[i] = -INFINITY;
-        ly[i] = INT_MAX;
-      }
-      if (ok && (!blank_by_am || p.fused)) {
-        float *frow = p.fused ? p.fused + rowoff : nullptr;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-          const int y0 = (c * kSlotLanes + g) * 4;
-          const uint4 w4 = *reinterpret_cast<const uint4 *>(win + y0);
-          const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
-          float kk[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int y = y0 + j;
-            const float x = xv[c][j];
-            float key = x;
-            if (y != blank) {
-              const uint32_t lo = ww[j] & 0xFFFFu, hi = ww[j] >> 16;
-              float lmv;
-              if (lo) {
-                lmv = lmval[y];
-              } else {
-                lmv = dv[c][j];
-#pragma unroll
-                for (int L2 = 2; L2 < kMaxLevels; ++L2)
-                  if (L2 <= m) lmv = lmv + bo[L2];
-              }
-              float bst = 0.0f;
-              if (p.has_trie) {
-                const float e = hi ? as_float(tr.delta[dbeg + (int)hi - 1].z) : rootE[y];
-                bst = e - phiq;
-              }
-              const float a1 = p.lam * lmv;
-              const float a2 = x + a1;
-              const float a3 = p.beta * bst;
-              key = a2 + a3;
-            }
-            kk[j] = key;
-            if (y < V && (p.mode == FUSION_BLANK_COMPETE || y != blank)) topk_insert<KM>(lk, ly, key, y);
-          }
-          if (frow) {
-            if (AL) {
-              if (y0 < V) *reinterpret_cast<float4 *>(frow + y0) = make_float4(kk[0] - lse, kk[1] - lse, kk[2] - lse, kk[3] - lse);
-            } else {
-#pragma unroll
-              for (int j = 0; j < 4; ++j)
-                if (y0 + j < V) frow[y0 + j] = kk[j] - lse;
-            }
+      for (int u = 0; u < kUD; ++u) {
+        const int j = u * W + g;
+        if (j < dcnt) {
+          win16[2 * dd[u].x + 1] = (uint16_t)(j + 1);
+          if (j < kAux) {
+            sE[j] = as_float(dd[u].z);
+            sDT[j] = dd[u].y;
           }
         }
       }
-      // ---- wave top-k by shuffles ---------------------------------------------
-      for (int j = 0; j < K; ++j) {
-        float bk = lk[0];
-        int by = ly[0];
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-          const float ok2 = __shfl_xor(bk, off);
-          const int oy = __shfl_xor(by, off);
-          if (before(ok2, oy, bk, by)) {
-            bk = ok2;
-            by = oy;
-          }
+      for (int j = kUD * W + g; j < dcnt; j += W) {
+        const int4 e = tr.delta[dbeg + j];
+        win16[2 * e.x + 1] = (uint16_t)(j + 1);
+        if (j < kAux) {
+          sE[j] = as_float(e.z);
+          sDT[j] = e.y;
         }
-        if (by != INT_MAX && ly[0] == by) {
+      }
+    }
+    const int nphase = N - 2 > 1 ? N - 2 : 1;
+    int covered = kUA * W;  // flattened arcs already fetched
+    for (int ph = 0; ph < nphase; ++ph) {
+      const int L = ph + 2;
+      if (ok && L <= m) {
 #pragma unroll
-          for (int i = 0; i < KM - 1; ++i) {
-            lk[i] = lk[i + 1];
-            ly[i] = ly[i + 1];
+        for (int u = 0; u < kUA; ++u)
+          if ((at[u] >> 16) == L) put_arc(L, at[u] & 0xFFFF, ab[u], tn[u]);
+        const int bL = rdl(rw, rec_beg_lane(L)), cL = rdl(rw, rec_cnt_lane(L));
+        const int done = min(cL, max(0, covered));
+        covered -= cL;
+        const int2 *A = s_arcs[L] + bL;
+        for (int j0 = done; j0 < cL; j0 += 4 * W) {
+          int2 a4[4];
+          int t4[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int j = j0 + u * W + g;
+            a4[u] = j < cL ? A[j] : make_int2(INT_MAX, 0);
+            t4[u] = (L == N - 1 && j < cL && j < kAux) ? lm.top_next[bL + j] : 0;
           }
-          lk[KM - 1] = -INFINITY;
-          ly[KM - 1] = INT_MAX;
-        }
-        if (lane == 0) {
-          s_wk[wave][j] = bk;
-          s_wy[wave][j] = by;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int j = j0 + u * W + g;
+            if (j < cL) put_arc(L, j, a4[u], t4[u]);
+          }
         }
       }
       __syncthreads();
-      // ---- slot top-k from the 4 wave lists, next states ------------------------
-      if (act && wslot == 0) {
-        if (!ok || blank_by_am) {
-          if (lane == 0) {
-            const float xb = xrow[blank];
-            s_cy[b][0] = blank;
-            s_cf[b][0] = xb - lse;
-            s_cl[b][0] = sig;
-            s_cq[b][0] = q;
-            s_cn[b] = 1;
-            if (!ok) atomicOr(&g_status, (ok_lm ? 0 : FUSION_STATUS_BAD_LM_STATE) | (ok_q ? 0 : FUSION_STATUS_BAD_BOOST_STATE));
+    }
+    // ---- keys, fused row, per-lane top-k, clear of the owned LDS entries --------
+    float M = -INFINITY, amx = -INFINITY, Ssum = 0.0f;
+    int am = INT_MAX;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_pm[w]);
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      if (s_pm[w] > -INFINITY) Ssum += s_ps[w] * expf(s_pm[w] - M);
+      if (s_pax[w] > amx || (s_pax[w] == amx && s_paid[w] < am)) {
+        amx = s_pax[w];
+        am = s_paid[w];
+      }
+    }
+    const float lse = M + logf(Ssum);
+    const bool blank_only = inv || (p.mode == FUSION_BLANK_AM && am == blank);
+    const bool want_keys = ok && (!blank_only || p.fused);
+    const bool write_fused = p.fused != nullptr && ok;
+    const rsrc_t fr = row_rsrc(write_fused ? p.fused + rowoff : p.logits, write_fused ? V : 0);
+    TopK<KM> tk;
+    tk.init();
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int y0 = (c * W + g) * 4;
+      const uint4 w4 = *reinterpret_cast<const uint4 *>(win + y0);
+      const float4 l4 = *reinterpret_cast<const float4 *>(lmval + y0);
+      const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
+      const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+      float kk[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int y = y0 + j;
+        const float x = xv[c][j];
+        const uint32_t lo = ww[j] & 0xFFFFu, hi = ww[j] >> 16;
+        // LM: the scattered value if an arc won, else the dense row plus the
+        // backoffs of levels 2.. (the +0.0 terms above m change nothing)
+        float dres = lv[j];
+#pragma unroll
+        for (int L2 = 2; L2 < kMaxLevels; ++L2) dres = dres + bo[L2];
+        const float lmv = lo ? lv[j] : dres;
+        // phrases: the transition's entry value if this state overrides y, else the root's
+        const int hidx = hi ? min((int)hi - 1, kAux - 1) : 0;
+        float e = hi ? sE[hidx] : rE[c][j];
+        if ((int)hi > kAux) e = as_float(tr.delta[dbeg + (int)hi - 1].z);
+        const float bst = e - phiq;
+        const float a1 = p.lam * lmv;
+        const float a2 = x + a1;
+        const float a3 = p.beta * (p.has_trie ? bst : 0.0f);
+        const float key = (y == blank) ? x : a2 + a3;
+        kk[j] = key;
+        const bool live_tok = act && y < V;
+        if (live_tok && blank_only && y == blank) tk.insert(x, blank, sid, qid);
+        if (live_tok && want_keys && !blank_only && (p.mode == FUSION_BLANK_COMPETE || y != blank) &&
+            tk.wants(key, y)) {
+          int nl = sid, nq = qid;
+          if (y != blank) {
+            nl = -1;
+            if (lo) {
+              const int L = (int)(lo >> 13), jj = (int)(lo & 0x1FFFu);
+              const int bL = s_lbeg[L];
+              const long long sb = s_sbase[L];
+              if (sb >= 0) nl = (int)(sb + bL + jj);
+              else nl = jj < kAux ? sTN[jj] : lm.top_next[bL + jj];
+            }
+            nq = -1;
+            if (hi) nq = (int)hi - 1 < kAux ? sDT[hi - 1] : tr.delta[dbeg + (int)hi - 1].y;
+            if (!p.has_trie) nq = 0;
           }
+          tk.insert(key, y, nl, nq);
+        }
+      }
+      *reinterpret_cast<uint4 *>(win + y0) = make_uint4(0u, 0u, 0u, 0u);
+      if (write_fused && y0 < V) {
+        if (AL) {
+          row_store4(fr, make_float4(kk[0] - lse, kk[1] - lse, kk[2] - lse, kk[3] - lse), voff, c * W * 16);
         } else {
-          const int ne = kWavesPerSlot * K;
-          float ek = -INFINITY;
-          int ey = INT_MAX;
-          if (lane < ne) {
-            ek = s_wk[slot * kWavesPerSlot + lane / K][lane % K];
-            ey = s_wy[slot * kWavesPerSlot + lane / K][lane % K];
-          }
-          int rank = 0, nvalid = 0;
-          for (int i = 0; i < ne; ++i) {
-            const float ok2 = s_wk[slot * kWavesPerSlot + i / K][i % K];
-            const int oy = s_wy[slot * kWavesPerSlot + i / K][i % K];
-            if (oy != INT_MAX) {
-              ++nvalid;
-              if (before(ok2, oy, ek, ey)) ++rank;
-            }
-          }
-          if (lane < ne && ey != INT_MAX && rank < K) {
-            const int y = ey;
-            int nl = sig, nq = q;
-            if (y != blank) {
-              const uint32_t w = win[y];
-              const uint32_t lo = w & 0xFFFFu, hi = w >> 16;
-              if (lo) {
-                const int L = (int)(lo >> 13), j = (int)(lo & 0x1FFFu);
-                int bL = 0;
 #pragma unroll
-                for (int L2 = 2; L2 < kMaxLevels; ++L2)
-                  if (L2 == L) bL = beg[L2];
-                const int64_t a = (int64_t)bL + j;
-                const long long sb = s_sbase[L];
-                nl = sb >= 0 ? (int)(sb + a) : lm.top_next[a];
-              } else {
-                nl = lm.dense_next[(int64_t)c1 * V + y];
-              }
-              nq = p.has_trie ? (hi ? tr.delta[dbeg + (int)hi - 1].y : tr.root_target[y]) : 0;
-            }
-            s_cy[b][rank] = y;
-            s_cf[b][rank] = ek - lse;
-            s_cl[b][rank] = nl;
-            s_cq[b][rank] = nq;
-          }
-          if (lane == 0) s_cn[b] = nvalid < K ? nvalid : K;
+          for (int j = 0; j < 4; ++j)
+            if (y0 + j < V) row_store1(fr, kk[j] - lse, voff + 4 * j, c * W * 16);
         }
-        if (p.traffic && lane == 0) {
-          unsigned long long by = 4ull * V;  // logits row
-          if (ok) {
-            const unsigned long long dense_row = 4ull * V;
-            by += umin64(8ull * (unsigned long long)lm.cnt1[c1], dense_row);
-#pragma unroll
-            for (int L2 = 2; L2 < kMaxLevels; ++L2)
-              if (L2 <= m) by += umin64(8ull * (unsigned long long)cnt[L2], dense_row) + 12ull;
-            if (m >= 2) by += 4ull;
-            if (p.has_trie) by += 16ull + 16ull * (unsigned long long)dcnt;
-          }
-          by += (B > 1) ? 8ull : 4ull;
-          if (p.fused) by += 4ull * V;
-          atomicAdd(&s_bytes, by);
-          atomicAdd(&s_steps, 1ull);
-        }
-      } else if (wslot == 0 && lane == 0 && b < B) {
-        s_cn[b] = 0;
       }
-      __syncthreads();
     }
-    // ---- selection across the stream ---------------------------------------------
-    if (p.step_mode) {
-      // fusion_step: B == 1, every candidate of the hypothesis is an output
-      if (tid < K) {
-        const int h = s;
-        const int n = s_cn[0];
-        const int64_t o = (int64_t)h * K + tid;
-        p.tokens[o] = tid < n ? s_cy[0][tid] : -1;
-        p.scores[o] = tid < n ? s_cf[0][tid] : -INFINITY;
-        p.next_lm[o] = tid < n ? s_cl[0][tid] : s_lm[0];
-        p.next_boost[o] = tid < n ? s_cq[0][tid] : s_q[0];
-      }
-    } else if (B == 1) {
-      if (tid == 0) {
-        const int y = s_cy[0][0];
-        p.tokens[(int64_t)t * H + s] = y;
-        n_lm[0] = s_cl[0][0];
-        n_q[0] = s_cq[0][0];
-        n_c1[0] = y != blank ? y : s_c1[0];
-        n_sc[0] = 0.0;
-      }
-    } else if (wave == 0) {
-      // beam: rank the live candidates by (score desc, parent asc, rank asc)
-      const int ncand = B * K;
-      int live = 0;
-      for (int i0 = 0; i0 < ncand; i0 += 64) {
-        const int i = i0 + lane;
-        bool valid = false;
-        double sc = -INFINITY;
-        int bi = 0, ji = 0;
-        if (i < ncand) {
-          bi = i / K;
-          ji = i % K;
-          valid = ji < s_cn[bi];
-          if (valid) sc = s_sc[bi] + (double)s_cf[bi][ji];
+    // ---- wave top-k by shuffles; the owning lane writes each winner ---------------
+    for (int j = 0; j < K; ++j) {
+      float bk = tk.k[0];
+      int by = tk.y[0];
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const float ok2 = __shfl_xor(bk, off);
+        const int oy = __shfl_xor(by, off);
+        if (before(ok2, oy, bk, by)) {
+          bk = ok2;
+          by = oy;
         }
-        int rank = 0;
-        if (valid) {
-          for (int i2 = 0; i2 < ncand; ++i2) {
-            const int b2 = i2 / K, j2 = i2 % K;
-            if (j2 >= s_cn[b2]) continue;
-            const double sc2 = s_sc[b2] + (double)s_cf[b2][j2];
-            if (sc2 > sc || (sc2 == sc && (b2 < bi || (b2 == bi && j2 < ji)))) ++rank;
+      }
+      if (by == INT_MAX) {
+        if (lane == 0) w_y[wave][j] = INT_MAX;
+      } else if (tk.y[0] == by) {
+        w_key[wave][j] = bk;
+        w_fus[wave][j] = bk - lse;
+        w_y[wave][j] = by;
+        w_lm[wave][j] = tk.lm[0];
+        w_q[wave][j] = tk.q[0];
+        tk.pop();
+      }
+    }
+    if (p.traffic && act && g == 0) {
+      unsigned long long by = 4ull * V;
+      if (ok) {
+        const unsigned long long row = 4ull * V;
+        by += umin64(8ull * (unsigned long long)lm.cnt1[c1], row);
+        for (int L2 = 2; L2 <= m; ++L2) by += umin64(8ull * (unsigned long long)rdl(rw, rec_cnt_lane(L2)), row) + 12ull;
+        if (m >= 2) by += 8ull;
+        if (p.has_trie) by += 16ull + 16ull * (unsigned long long)dcnt;
+      }
+      by += B > 1 ? 8ull : 4ull;
+      if (p.fused) by += 4ull * V;
+      s_bytes += by;
+      s_steps += 1ull;
+    }
+    __syncthreads();
+    // ---- the hypothesis' top-k (wave 0): the rank of every wave entry ------------------
+    if (wave == 0) {
+      const int ne = NW * K;  // <= 128: at most two entries per lane
+      float c_f[2];
+      int c_y[2], c_l[2], c_q[2], c_r[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int i = lane + 64 * u;
+        c_r[u] = INT_MAX;
+        c_f[u] = 0.0f;
+        c_y[u] = INT_MAX;
+        c_l[u] = 0;
+        c_q[u] = 0;
+        if (i < ne) {
+          const int w = i / K, j = i % K;
+          const int y = w_y[w][j];
+          if (y != INT_MAX) {
+            const float key = w_key[w][j];
+            int r = 0;
+            for (int i2 = 0; i2 < ne; ++i2) {
+              const int y2 = w_y[i2 / K][i2 % K];
+              if (y2 != INT_MAX && before(w_key[i2 / K][i2 % K], y2, key, y)) ++r;
+            }
+            c_r[u] = r;
+            c_f[u] = w_fus[w][j];
+            c_y[u] = y;
+            c_l[u] = w_lm[w][j];
+            c_q[u] = w_q[w][j];
           }
-          if (rank < B) {
-            const int y = s_cy[bi][ji];
-            n_lm[rank] = s_cl[bi][ji];
-            n_q[rank] = s_cq[bi][ji];
-            n_c1[rank] = y != blank ? y : s_c1[bi];
-            n_sc[rank] = sc;
-            const int64_t o = (int64_t)t * H + (int64_t)s * B + rank;
+        }
+      }
+      // candidate j of this hypothesis = the entry of rank j
+      auto cand = [&](int j, float &f, int &y, int &l, int &q) {
+        int found = -1;
+        f = -INFINITY;
+        y = INT_MAX;
+        l = 0;
+        q = 0;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+          if (c_r[u] == j) found = u;
+        const unsigned long long bal = __ballot(found >= 0);
+        if (bal) {
+          const int src = __ffsll((long long)bal) - 1;
+          const int u = __shfl(found, src);
+          const float f0 = __shfl(c_f[0], src), f1 = __shfl(c_f[1], src);
+          const int y0 = __shfl(c_y[0], src), y1 = __shfl(c_y[1], src);
+          const int l0 = __shfl(c_l[0], src), l1 = __shfl(c_l[1], src);
+          const int q0 = __shfl(c_q[0], src), q1 = __shfl(c_q[1], src);
+          f = u ? f1 : f0;
+          y = u ? y1 : y0;
+          l = u ? l1 : l0;
+          q = u ? q1 : q0;
+        }
+      };
+      if (p.step_mode) {
+        for (int j = 0; j < K; ++j) {
+          float f;
+          int y, l, q;
+          cand(j, f, y, l, q);
+          if (lane == 0) {
+            const int64_t o = (int64_t)h * K + j;
+            if (y == INT_MAX) {
+              p.tokens[o] = -1;
+              p.scores[o] = -INFINITY;
+              p.next_lm[o] = hs.cur_lm;
+              p.next_boost[o] = hs.cur_q;
+            } else {
+              if (!inv && l < 0) l = lm.rec_dense[((int64_t)hs.c1 * V + y) * RS + 1];
+              if (!inv && q < 0) q = tr.root_node[y].w;
+              p.tokens[o] = y;
+              p.scores[o] = f;
+              p.next_lm[o] = l;
+              p.next_boost[o] = q;
+            }
+          }
+        }
+      } else if (B == 1) {
+        float f;
+        int y, l, q;
+        cand(0, f, y, l, q);
+        if (lane == 0) {
+          p.tokens[(int64_t)t * H + h] = y;
+          const int c1p = hs.c1;
+          hs.lmsrc = l;
+          hs.qsrc = q;
+          hs.y = y;
+          hs.c1p = c1p;
+          hs.c1 = y != blank ? y : c1p;
+        }
+      } else {
+        // ---- beam: publish this hypothesis' candidates, meet the stream, rank all ----
+        int4 *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * 2;
+        const double S0 = hs.S;
+        const int c1_now = hs.c1, fl_now = hs.fl;
+        for (int j = 0; j < K; ++j) {
+          float f;
+          int y, l, q;
+          cand(j, f, y, l, q);
+          if (lane == 0) {
+            if (!act) y = INT_MAX;
+            xs[(b * K + j) * 2] = make_int4(as_int(f), y, l, q);
+            xs[(b * K + j) * 2 + 1] = make_int4(c1_now, fl_now, __double2loint(S0), __double2hiint(S0));
+          }
+        }
+        int *cnt = p.counters + (size_t)sl * kCounterStride;
+        if (lane == 0) {
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+          __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const int target = B * (t + 1);
+          int spins = 0;
+          while (!aborted && __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            if (++spins > kSpinLimit) {
+              atomicOr(&g_status, FUSION_STATUS_SYNC_TIMEOUT);
+              aborted = true;
+            }
+            __builtin_amdgcn_s_sleep(1);
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        // every workgroup of the stream ranks the same B*k candidates by
+        // (running score + fused desc, parent asc, rank asc); slot b takes rank b
+        const int nc = B * K;
+        int hit = 0, rl = 0, rq = 0, ry = 0, rc1 = 0, rfl = 0, rlo = 0, rhi = 0, rpar = 0;
+        for (int i0 = 0; i0 < nc; i0 += 64) {
+          const int i = i0 + lane;
+          int4 a = make_int4(0, INT_MAX, 0, 0), bb = make_int4(0, 0, 0, 0);
+          if (i < nc) {
+            a = xs[i * 2];
+            bb = xs[i * 2 + 1];
+          }
+          const bool valid = i < nc && a.y != INT_MAX;
+          const double sc = valid ? __hiloint2double(bb.w, bb.z) + (double)as_float(a.x) : -INFINITY;
+          int r = 0;
+          for (int i2 = 0; i2 < nc; ++i2) {
+            const int src = i2 & 63;
+            // candidates of this 64-block are in registers; others are re-read
+            double sc2;
+            int v2;
+            if ((i2 >> 6) == (i0 >> 6)) {
+              sc2 = __shfl(sc, src);
+              v2 = __shfl((int)valid, src);
+            } else {
+              const int4 a2 = xs[i2 * 2];
+              const int4 b2 = xs[i2 * 2 + 1];
+              v2 = a2.y != INT_MAX;
+              sc2 = __hiloint2double(b2.w, b2.z) + (double)as_float(a2.x);
+            }
+            if (v2 && (sc2 > sc || (sc2 == sc && i2 < i))) ++r;
+          }
+          if (valid && r == b) {
+            hit = 1;
+            ry = a.y;
+            rl = a.z;
+            rq = a.w;
+            rc1 = bb.x;
+            rfl = bb.y;
+            rlo = __double2loint(sc);
+            rhi = __double2hiint(sc);
+            rpar = i / K;
+          }
+        }
+        const unsigned long long bal = __ballot(hit);
+        const int64_t o = (int64_t)t * H + h;
+        if (bal) {
+          const int src = __ffsll((long long)bal) - 1;
+          const int y = __shfl(ry, src), l = __shfl(rl, src), q = __shfl(rq, src);
+          const int c1p = __shfl(rc1, src), pfl = __shfl(rfl, src);
+          const int slo = __shfl(rlo, src), shi = __shfl(rhi, src), par = __shfl(rpar, src);
+          if (lane == 0) {
+            hs.lmsrc = l;
+            hs.qsrc = q;
+            hs.y = y;
+            hs.c1p = c1p;
+            hs.c1 = y != blank ? y : c1p;
+            hs.fl = 1 | (pfl & 2);
+            hs.S = __hiloint2double(shi, slo);
             p.tokens[o] = y;
-            p.parents[o] = bi;
+            p.parents[o] = par;
           }
+        } else if (lane == 0) {
+          // no candidate reaches this slot: the hypothesis is dead and keeps its state
+          hs.lmsrc = hs.cur_lm;
+          hs.qsrc = hs.cur_q;
+          hs.y = -1;
+          hs.c1p = -1;
+          hs.fl = 0;
+          hs.S = -INFINITY;
+          p.tokens[o] = -1;
+          p.parents[o] = -1;
         }
-        live += __popcll(__ballot(valid));
-      }
-      for (int i = live + lane; i < B; i += 64) {
-        n_lm[i] = s_lm[i];
-        n_q[i] = s_q[i];
-        n_c1[i] = s_c1[i];
-        n_sc[i] = -INFINITY;
-        const int64_t o = (int64_t)t * H + (int64_t)s * B + i;
-        p.tokens[o] = -1;
-        p.parents[o] = -1;
       }
     }
     __syncthreads();
-    if (!p.step_mode && tid < B) {
-      s_lm[tid] = n_lm[tid];
-      s_q[tid] = n_q[tid];
-      s_c1[tid] = n_c1[tid];
-      s_sc[tid] = n_sc[tid];
-    }
-    __syncthreads();
   }
-  // ---- final states ------------------------------------------------------------------
-  if (!p.step_mode && tid < B) {
-    const int h = s * B + tid;
-    p.lm_state[h] = s_lm[tid];
-    if (p.has_trie) p.boost_state[h] = s_q[tid];
-    if (B > 1) p.hyp_score[h] = s_sc[tid];
+  // ---- final state ----------------------------------------------------------------
+  if (!p.step_mode && g == 0) {
+    const int V = p.V;
+    int nl = hs.lmsrc, nq = hs.qsrc;
+    const int y = hs.y;
+    // a negative source means "reached by token y" only for valid hypotheses
+    // that made a transition; an invalid hypothesis keeps its raw ids
+    const bool moved = (hs.fl & 2) == 0 && y >= 0 && y != p.blank;
+    if (moved && nl < 0) nl = lm.rec_dense[((int64_t)hs.c1p * V + y) * RS + 1];
+    if (moved && nq < 0) nq = tr.root_node[y].w;
+    p.lm_state[h] = nl;
+    if (p.has_trie) p.boost_state[h] = nq;
+    if (B > 1) p.hyp_score[h] = hs.S;
   }
-  if (p.traffic && tid == 0) {
-    unsigned long long extra = (s == 0 && p.has_trie) ? 4ull * V * (unsigned long long)p.T : 0ull;
+  if (p.traffic && g == 0) {
+    const unsigned long long extra = (h == 0 && p.has_trie) ? 4ull * p.V * (unsigned long long)p.T : 0ull;
     atomicAdd(reinterpret_cast<unsigned long long *>(p.traffic), s_bytes + extra);
     atomicAdd(reinterpret_cast<unsigned long long *>(p.traffic) + 1, s_steps);
   }
+}
+
+__global__ void zero_ints(int *p, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -578,70 +839,113 @@ __global__ void __launch_bounds__(NC >= 8 ? 512 : 1024) fusion_kernel(Params p) 
 // ---------------------------------------------------------------------------
 typedef void (*KernelFn)(Params);
 
-template <int NC, int KM>
+template <int W, int NC, int KM>
 KernelFn pick_al(bool al) {
-  return al ? fusion_kernel<NC, KM, true> : fusion_kernel<NC, KM, false>;
+  return al ? fusion_kernel<W, NC, KM, true> : fusion_kernel<W, NC, KM, false>;
 }
-template <int NC>
+template <int W, int NC>
 KernelFn pick_k(int km, bool al) {
-  return km == 1 ? pick_al<NC, 1>(al) : km == 4 ? pick_al<NC, 4>(al) : pick_al<NC, 8>(al);
-}
-KernelFn pick(int nc, int km, bool al) {
-  switch (nc) {
-    case 1: return pick_k<1>(km, al);
-    case 2: return pick_k<2>(km, al);
-    case 4: return pick_k<4>(km, al);
-    default: return pick_k<8>(km, al);
-  }
+  return km == 1 ? pick_al<W, NC, 1>(al) : km == 4 ? pick_al<W, NC, 4>(al) : pick_al<W, NC, 8>(al);
 }
 
-struct DeviceLimits {
-  int lds_per_block = 0;
+struct Shape {
+  int W, NC, Vp;
+};
+
+// lanes per hypothesis and 4-token strips per lane for a vocabulary
+Shape shape_for(int V) {
+  if (V <= 256) return {64, 1, 256};
+  if (V <= 1024) return {256, 1, 1024};
+  if (V <= 4096) return {1024, 1, 4096};
+  return {1024, 2, 8192};
+}
+
+KernelFn pick(const Shape &sh, int km, bool al) {
+  if (sh.W == 64) return pick_k<64, 1>(km, al);
+  if (sh.W == 256) return pick_k<256, 1>(km, al);
+  if (sh.NC == 1) return pick_k<1024, 1>(km, al);
+  return pick_k<1024, 2>(km, al);
+}
+
+struct DeviceInfo {
+  int lds_per_block = 0, cus = 0;
   bool ok = false;
 };
 
-DeviceLimits device_limits() {
+DeviceInfo device_info() {
   static std::mutex mu;
-  static DeviceLimits cache[64];
+  static DeviceInfo cache[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return {};
   std::lock_guard<std::mutex> lk(mu);
   if (!cache[dev].ok) {
-    int v = 0;
+    int v = 0, c = 0;
     if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) return {};
+    if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return {};
     cache[dev].lds_per_block = v;
+    cache[dev].cus = c;
     cache[dev].ok = true;
   }
   return cache[dev];
 }
 
-int launch(Params &p, int grid, hipStream_t stream) {
-  const int nc_need = (p.V + 1023) / 1024;
-  const int nc = nc_need <= 1 ? 1 : nc_need <= 2 ? 2 : nc_need <= 4 ? 4 : 8;
+int launch(Params &p, int n_hyp, hipStream_t stream) {
+  const Shape sh = shape_for(p.V);
   const int km = p.k <= 1 ? 1 : p.k <= 4 ? 4 : 8;
   const bool al = (p.V % 4 == 0) && ((uintptr_t)p.logits % 16 == 0) && (!p.fused || (uintptr_t)p.fused % 16 == 0);
-  KernelFn fn = pick(nc, km, al);
+  KernelFn fn = pick(sh, km, al);
+  const DeviceInfo di = device_info();
+  if (!di.ok) return set_error(FUSION_E_HIP, "cannot query the device");
+  const size_t dyn = (size_t)4 * (2 * sh.Vp + 3 * kAux);
   hipFuncAttributes attr;
   hipError_t e = hipFuncGetAttributes(&attr, reinterpret_cast<const void *>(fn));
   if (e != hipSuccess) return hip_error(e, "hipFuncGetAttributes");
-  DeviceLimits lim = device_limits();
-  if (!lim.ok) return set_error(FUSION_E_HIP, "cannot query the device's LDS size");
-  p.Vp = nc * 1024;
-  const size_t per_slot = (size_t)8 * p.Vp;
-  const size_t fixed = (size_t)4 * p.Vp;  // root row
-  const long lds_avail = (long)lim.lds_per_block - (long)attr.sharedSizeBytes - (long)fixed;
-  int slots = (int)std::min<size_t>((size_t)kMaxSlots, lds_avail > 0 ? (size_t)lds_avail / per_slot : 0);
-  if (nc >= 8) slots = std::min(slots, 2);
-  slots = std::min(slots, p.B);
-  if (slots < 1) return set_error(FUSION_E_UNSUPPORTED, "vocabulary too large for the device's LDS");
-  p.slots = slots;
-  const size_t dyn = per_slot * slots + fixed;
+  if (dyn + attr.sharedSizeBytes > (size_t)di.lds_per_block)
+    return set_error(FUSION_E_UNSUPPORTED, "vocabulary too large for the device's LDS");
   e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn), hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
   if (e != hipSuccess) return hip_error(e, "hipFuncSetAttribute");
-  hipLaunchKernelGGL(fn, dim3(grid), dim3(slots * kSlotLanes), dyn, stream, p);
-  e = hipGetLastError();
-  if (e != hipSuccess) return hip_error(e, "fusion kernel launch");
-  return FUSION_OK;
+  p.s_off = 0;
+  p.xcd_map = 0;
+  if (p.B == 1 || p.step_mode) {
+    hipLaunchKernelGGL(fn, dim3(n_hyp), dim3(sh.W), dyn, stream, p);
+    e = hipGetLastError();
+    return e == hipSuccess ? FUSION_OK : hip_error(e, "fusion kernel launch");
+  }
+  // beam: every workgroup of a stream must be resident together (cooperative
+  // launch); streams beyond what fits at once run in further launches
+  int per_cu = 0;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(fn), sh.W, dyn);
+  if (e != hipSuccess) return hip_error(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+  const long resident = (long)per_cu * di.cus;
+  int s_batch = (int)std::min<long>(p.S, resident / p.B);
+  if (s_batch >= 8) s_batch -= s_batch % 8;
+  if (s_batch < 1) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device at once");
+  const size_t xbytes = (size_t)s_batch * 2 * p.B * p.k * 2 * sizeof(int4);
+  const size_t cbytes = (size_t)s_batch * kCounterStride * sizeof(int);
+  void *scratch = nullptr;
+  e = hipMallocAsync(&scratch, xbytes + cbytes, stream);
+  if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
+  p.xchg = reinterpret_cast<int4 *>(scratch);
+  p.counters = reinterpret_cast<int *>(reinterpret_cast<char *>(scratch) + xbytes);
+  int rc = FUSION_OK;
+  for (int s0 = 0; s0 < p.S && rc == FUSION_OK; s0 += s_batch) {
+    const int ns = std::min(s_batch, p.S - s0);
+    hipLaunchKernelGGL(zero_ints, dim3(1), dim3(256), 0, stream, p.counters, s_batch * kCounterStride);
+    e = hipGetLastError();
+    if (e != hipSuccess) {
+      rc = hip_error(e, "counter reset launch");
+      break;
+    }
+    Params q = p;
+    q.s_off = s0;
+    q.xcd_map = (ns % 8 == 0) ? 1 : 0;
+    void *args[] = {&q};
+    e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(ns * p.B), dim3(sh.W), args, dyn, stream);
+    if (e != hipSuccess) rc = hip_error(e, "cooperative fusion kernel launch");
+  }
+  hipError_t e2 = hipFreeAsync(scratch, stream);
+  if (rc == FUSION_OK && e2 != hipSuccess) rc = hip_error(e2, "hipFreeAsync");
+  return rc;
 }
 
 int check_common(const NgramTables *lm, const BoostTrie *trie, const float *logits, int32_t V,
@@ -754,5 +1058,5 @@ extern "C" int fusion_run(const NgramTables *lm, const BoostTrie *trie, const fl
   p.step_mode = 0;
   p.lam = lambda;
   p.beta = beta;
-  return launch(p, S, stream);
+  return launch(p, S * B, stream);
 }

@@ -213,7 +213,7 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
   const int RS = d.rec_stride;
   // ---- dense level-1 rows ----------------------------------------------------
   std::vector<float> dense((size_t)(V + 2) * V);
-  std::vector<int32_t> dense_next((size_t)(V + 2) * V);
+  std::vector<int32_t> dense_next((size_t)(V + 2) * V);  // host only: state after (w, y)
   std::vector<int32_t> cnt1(V + 2, 0);
   std::vector<int64_t> uni_row(V + 2, -1);
   for (int64_t i = 0; i < ord[1].n; ++i) uni_row[tok_of(1, i, 0)] = i;
@@ -264,22 +264,37 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
       for (int64_t i = a; i < e; ++i) {
         int32_t *r = rec.data() + (size_t)(d.off[m] - (V + 2) + i) * RS;
         r[0] = tok_of(m, i, m - 1) | (m << 16);
+        r[1] = (int32_t)(d.off[m] + i);
         if (m >= 3) {
           const int32_t *sr = rec.data() + (size_t)(d.off[m - 1] - (V + 2) + sfx[m][i]) * RS;
-          std::memcpy(r + 1, sr + 1, sizeof(int32_t) * 3 * (m - 2));
+          std::memcpy(r + 2, sr + 2, sizeof(int32_t) * 3 * (m - 2));
         }
         float bo = bo_of(m, i);
-        std::memcpy(&r[1 + 3 * (m - 2)], &bo, 4);
-        r[1 + 3 * (m - 2) + 1] = (int32_t)arc_beg[m][i];
-        r[1 + 3 * (m - 2) + 2] = (int32_t)arc_cnt[m][i];
+        std::memcpy(&r[2 + 3 * (m - 2)], &bo, 4);
+        r[2 + 3 * (m - 2) + 1] = (int32_t)arc_beg[m][i];
+        r[2 + 3 * (m - 2) + 2] = (int32_t)arc_cnt[m][i];
       }
     });
   }
+  // ---- record of the state after (w, y) for every one-token context w ------
+  std::vector<int32_t> rec_dense((size_t)(V + 2) * V * RS, 0);
+  parallel_for((int64_t)(V + 2) * V, [&](int64_t a, int64_t e) {
+    for (int64_t i = a; i < e; ++i) {
+      const int32_t sid = dense_next[i];
+      int32_t *r = rec_dense.data() + (size_t)i * RS;
+      if (sid >= V + 2) {
+        std::memcpy(r, rec.data() + (size_t)(sid - (V + 2)) * RS, sizeof(int32_t) * RS);
+      } else {
+        r[0] = sid | (1 << 16);
+        r[1] = sid;
+      }
+    }
+  });
   // ---- upload -------------------------------------------------------------------
   DeviceUpload up{t, stream};
   int rc = FUSION_OK;
   if (rc == FUSION_OK) rc = up.put(dense, &d.dense);
-  if (rc == FUSION_OK) rc = up.put(dense_next, &d.dense_next);
+  if (rc == FUSION_OK) rc = up.put(rec_dense, &d.rec_dense);
   if (rc == FUSION_OK) rc = up.put(cnt1, &d.cnt1);
   if (rc == FUSION_OK) rc = up.put(rec, &d.rec);
   for (int L = 2; L <= N - 1 && rc == FUSION_OK; ++L) rc = up.put(arcs[L], &d.arcs[L]);
