@@ -118,35 +118,33 @@ __device__ __forceinline__ int rec_bo_lane(int L) { return 2 + 3 * (L - 2); }
 __device__ __forceinline__ int rec_beg_lane(int L) { return 3 + 3 * (L - 2); }
 __device__ __forceinline__ int rec_cnt_lane(int L) { return 4 + 3 * (L - 2); }
 
-// sorted per-lane candidate list: key desc, id asc; each entry carries where
-// the state after that token comes from (LM: state id, or -1 = the record at
-// (c_1, y); phrases: node id, or -1 = the root transition of y)
+// sorted per-lane candidate list: key desc, id asc; an entry keeps the token's
+// LDS tag word (LM winner level/offset, phrase transition) so that only the
+// winners resolve where their next state comes from
 template <int KM>
 struct TopK {
   float k[KM];
-  int y[KM], lm[KM], q[KM];
+  int y[KM];
+  uint32_t w[KM];
   __device__ __forceinline__ void init() {
 #pragma unroll
     for (int i = 0; i < KM; ++i) {
       k[i] = -INFINITY;
       y[i] = INT_MAX;
-      lm[i] = 0;
-      q[i] = 0;
+      w[i] = 0u;
     }
   }
   __device__ __forceinline__ bool wants(float key, int yy) const { return before(key, yy, k[KM - 1], y[KM - 1]); }
-  __device__ __forceinline__ void insert(float key, int yy, int l, int qq) {
+  __device__ __forceinline__ void insert(float key, int yy, uint32_t ww) {
     k[KM - 1] = key;
     y[KM - 1] = yy;
-    lm[KM - 1] = l;
-    q[KM - 1] = qq;
+    w[KM - 1] = ww;
 #pragma unroll
     for (int i = KM - 1; i > 0; --i) {
       if (before(k[i], y[i], k[i - 1], y[i - 1])) {
         float tk = k[i]; k[i] = k[i - 1]; k[i - 1] = tk;
         int ty = y[i]; y[i] = y[i - 1]; y[i - 1] = ty;
-        int tl = lm[i]; lm[i] = lm[i - 1]; lm[i - 1] = tl;
-        int tq = q[i]; q[i] = q[i - 1]; q[i - 1] = tq;
+        uint32_t tw = w[i]; w[i] = w[i - 1]; w[i - 1] = tw;
       }
     }
   }
@@ -155,13 +153,38 @@ struct TopK {
     for (int i = 0; i < KM - 1; ++i) {
       k[i] = k[i + 1];
       y[i] = y[i + 1];
-      lm[i] = lm[i + 1];
-      q[i] = q[i + 1];
+      w[i] = w[i + 1];
     }
     k[KM - 1] = -INFINITY;
     y[KM - 1] = INT_MAX;
   }
 };
+
+// ---- wave-level argmax over (key desc, id asc) with DPP moves (no LDS) --------
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void dpp_best(float &k, int &y) {
+  const float k2 = __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY), __float_as_int(k), CTRL, ROWS, 0xF, false));
+  const int y2 = __builtin_amdgcn_update_dpp(INT_MAX, y, CTRL, ROWS, 0xF, false);
+  if (before(k2, y2, k, y)) {
+    k = k2;
+    y = y2;
+  }
+}
+// every lane of each 16-lane row ends with the row's best
+__device__ __forceinline__ void row_best(float &k, int &y) {
+  dpp_best<0xB1, 0xF>(k, y);   // quad_perm [1,0,3,2]
+  dpp_best<0x4E, 0xF>(k, y);   // quad_perm [2,3,0,1]
+  dpp_best<0x141, 0xF>(k, y);  // row_half_mirror
+  dpp_best<0x140, 0xF>(k, y);  // row_mirror
+}
+// the wave's best, returned uniformly (lane 63 holds it after the row broadcasts)
+__device__ __forceinline__ void wave_best(float k, int y, float &bk, int &by) {
+  row_best(k, y);
+  dpp_best<0x142, 0xA>(k, y);  // row_bcast:15 -> rows 1, 3
+  dpp_best<0x143, 0xC>(k, y);  // row_bcast:31 -> rows 2, 3
+  bk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(k), 63));
+  by = __builtin_amdgcn_readlane(y, 63);
+}
 
 // hypothesis state carried between frames (LDS, written by one lane)
 struct HypState {
@@ -186,8 +209,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   int *sTN = sDT + kAux;
   __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves], s_pax[kMaxWaves];
   __shared__ int s_paid[kMaxWaves];
-  __shared__ float w_key[kMaxWaves][KM], w_fus[kMaxWaves][KM];
-  __shared__ int w_y[kMaxWaves][KM], w_lm[kMaxWaves][KM], w_q[kMaxWaves][KM];
+  __shared__ float w_key[kMaxWaves][KM];
+  __shared__ int w_y[kMaxWaves][KM];
+  __shared__ uint32_t w_tag[kMaxWaves][KM];
   __shared__ HypState hs;
   __shared__ const int2 *s_arcs[kMaxLevels];
   __shared__ long long s_sbase[kMaxLevels];
@@ -543,25 +567,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const float key = (y == blank) ? x : a2 + a3;
         kk[j] = key;
         const bool live_tok = act && y < V;
-        if (live_tok && blank_only && y == blank) tk.insert(x, blank, sid, qid);
+        if (live_tok && blank_only && y == blank) tk.insert(x, blank, 0u);
         if (live_tok && want_keys && !blank_only && (p.mode == FUSION_BLANK_COMPETE || y != blank) &&
-            tk.wants(key, y)) {
-          int nl = sid, nq = qid;
-          if (y != blank) {
-            nl = -1;
-            if (lo) {
-              const int L = (int)(lo >> 13), jj = (int)(lo & 0x1FFFu);
-              const int bL = s_lbeg[L];
-              const long long sb = s_sbase[L];
-              if (sb >= 0) nl = (int)(sb + bL + jj);
-              else nl = jj < kAux ? sTN[jj] : lm.top_next[bL + jj];
-            }
-            nq = -1;
-            if (hi) nq = (int)hi - 1 < kAux ? sDT[hi - 1] : tr.delta[dbeg + (int)hi - 1].y;
-            if (!p.has_trie) nq = 0;
-          }
-          tk.insert(key, y, nl, nq);
-        }
+            tk.wants(key, y))
+          tk.insert(key, y, ww[j]);
       }
       *reinterpret_cast<uint4 *>(win + y0) = make_uint4(0u, 0u, 0u, 0u);
       if (write_fused && y0 < V) {
@@ -574,27 +583,17 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
       }
     }
-    // ---- wave top-k by shuffles; the owning lane writes each winner ---------------
+    // ---- wave top-k (DPP argmax, K rounds); the owning lane writes each winner -----
     for (int j = 0; j < K; ++j) {
-      float bk = tk.k[0];
-      int by = tk.y[0];
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        const float ok2 = __shfl_xor(bk, off);
-        const int oy = __shfl_xor(by, off);
-        if (before(ok2, oy, bk, by)) {
-          bk = ok2;
-          by = oy;
-        }
-      }
+      float bk;
+      int by;
+      wave_best(tk.k[0], tk.y[0], bk, by);
       if (by == INT_MAX) {
         if (lane == 0) w_y[wave][j] = INT_MAX;
       } else if (tk.y[0] == by) {
         w_key[wave][j] = bk;
-        w_fus[wave][j] = bk - lse;
         w_y[wave][j] = by;
-        w_lm[wave][j] = tk.lm[0];
-        w_q[wave][j] = tk.q[0];
+        w_tag[wave][j] = tk.w[0];
         tk.pop();
       }
     }
@@ -613,114 +612,104 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       s_steps += 1ull;
     }
     __syncthreads();
-    // ---- the hypothesis' top-k (wave 0): the rank of every wave entry ------------------
+    // ---- the hypothesis' top-k (wave 0): K DPP rounds over the NW sorted wave lists --
     if (wave == 0) {
-      const int ne = NW * K;  // <= 128: at most two entries per lane
-      float c_f[2];
-      int c_y[2], c_l[2], c_q[2], c_r[2];
+      // lane w < NW holds wave w's list (best first)
+      float hk[KM];
+      int hy[KM];
+      uint32_t hw[KM];
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int i = lane + 64 * u;
-        c_r[u] = INT_MAX;
-        c_f[u] = 0.0f;
-        c_y[u] = INT_MAX;
-        c_l[u] = 0;
-        c_q[u] = 0;
-        if (i < ne) {
-          const int w = i / K, j = i % K;
-          const int y = w_y[w][j];
-          if (y != INT_MAX) {
-            const float key = w_key[w][j];
-            int r = 0;
-            for (int i2 = 0; i2 < ne; ++i2) {
-              const int y2 = w_y[i2 / K][i2 % K];
-              if (y2 != INT_MAX && before(w_key[i2 / K][i2 % K], y2, key, y)) ++r;
-            }
-            c_r[u] = r;
-            c_f[u] = w_fus[w][j];
-            c_y[u] = y;
-            c_l[u] = w_lm[w][j];
-            c_q[u] = w_q[w][j];
+      for (int j = 0; j < KM; ++j) {
+        const bool have = lane < NW && j < K;
+        hy[j] = have ? w_y[lane][j] : INT_MAX;
+        hk[j] = (have && hy[j] != INT_MAX) ? w_key[lane][j] : -INFINITY;
+        hw[j] = have ? w_tag[lane][j] : 0u;
+      }
+      // candidate j ends in lane j
+      float ck = -INFINITY;
+      int cy = INT_MAX;
+      uint32_t cw = 0u;
+      for (int j = 0; j < K; ++j) {
+        float k = hk[0];
+        int y = hy[0];
+        row_best(k, y);
+        const float bk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(k), 0));
+        const int by = __builtin_amdgcn_readlane(y, 0);
+        if (by == INT_MAX) break;
+        const unsigned long long own = __ballot(hy[0] == by && lane < NW);
+        const int src = __ffsll((long long)own) - 1;
+        const uint32_t wsrc = (uint32_t)__builtin_amdgcn_readlane((int)hw[0], src);
+        if (lane == j) {
+          ck = bk;
+          cy = by;
+          cw = wsrc;
+        }
+        if (lane == src) {
+#pragma unroll
+          for (int i = 0; i < KM - 1; ++i) {
+            hk[i] = hk[i + 1];
+            hy[i] = hy[i + 1];
+            hw[i] = hw[i + 1];
           }
+          hk[KM - 1] = -INFINITY;
+          hy[KM - 1] = INT_MAX;
         }
       }
-      // candidate j of this hypothesis = the entry of rank j
-      auto cand = [&](int j, float &f, int &y, int &l, int &q) {
-        int found = -1;
-        f = -INFINITY;
-        y = INT_MAX;
-        l = 0;
-        q = 0;
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-          if (c_r[u] == j) found = u;
-        const unsigned long long bal = __ballot(found >= 0);
-        if (bal) {
-          const int src = __ffsll((long long)bal) - 1;
-          const int u = __shfl(found, src);
-          const float f0 = __shfl(c_f[0], src), f1 = __shfl(c_f[1], src);
-          const int y0 = __shfl(c_y[0], src), y1 = __shfl(c_y[1], src);
-          const int l0 = __shfl(c_l[0], src), l1 = __shfl(c_l[1], src);
-          const int q0 = __shfl(c_q[0], src), q1 = __shfl(c_q[1], src);
-          f = u ? f1 : f0;
-          y = u ? y1 : y0;
-          l = u ? l1 : l0;
-          q = u ? q1 : q0;
+      // each candidate lane resolves where its next state comes from (see HypState)
+      const float cf = ck - lse;
+      int cl = sid, cq = qid;
+      if (cy != INT_MAX && cy != blank) {
+        const uint32_t lo = cw & 0xFFFFu, hi = cw >> 16;
+        cl = -1;
+        if (lo) {
+          const int L = (int)(lo >> 13), jj = (int)(lo & 0x1FFFu);
+          const int bL = s_lbeg[L];
+          const long long sb = s_sbase[L];
+          cl = sb >= 0 ? (int)(sb + bL + jj) : (jj < kAux ? sTN[jj] : lm.top_next[bL + jj]);
         }
-      };
+        cq = -1;
+        if (hi) cq = (int)hi - 1 < kAux ? sDT[hi - 1] : tr.delta[dbeg + (int)hi - 1].y;
+        if (!p.has_trie) cq = 0;
+      }
       if (p.step_mode) {
-        for (int j = 0; j < K; ++j) {
-          float f;
-          int y, l, q;
-          cand(j, f, y, l, q);
-          if (lane == 0) {
-            const int64_t o = (int64_t)h * K + j;
-            if (y == INT_MAX) {
-              p.tokens[o] = -1;
-              p.scores[o] = -INFINITY;
-              p.next_lm[o] = hs.cur_lm;
-              p.next_boost[o] = hs.cur_q;
-            } else {
-              if (!inv && l < 0) l = lm.rec_dense[((int64_t)hs.c1 * V + y) * RS + 1];
-              if (!inv && q < 0) q = tr.root_node[y].w;
-              p.tokens[o] = y;
-              p.scores[o] = f;
-              p.next_lm[o] = l;
-              p.next_boost[o] = q;
-            }
+        if (lane < K) {
+          const int64_t o = (int64_t)h * K + lane;
+          if (cy == INT_MAX) {
+            p.tokens[o] = -1;
+            p.scores[o] = -INFINITY;
+            p.next_lm[o] = hs.cur_lm;
+            p.next_boost[o] = hs.cur_q;
+          } else {
+            int l = cl, q = cq;
+            if (!inv && l < 0) l = lm.rec_dense[((int64_t)hs.c1 * V + cy) * RS + 1];
+            if (!inv && q < 0) q = tr.root_node[cy].w;
+            p.tokens[o] = cy;
+            p.scores[o] = cf;
+            p.next_lm[o] = l;
+            p.next_boost[o] = q;
           }
         }
       } else if (B == 1) {
-        float f;
-        int y, l, q;
-        cand(0, f, y, l, q);
         if (lane == 0) {
-          p.tokens[(int64_t)t * H + h] = y;
+          p.tokens[(int64_t)t * H + h] = cy;
           const int c1p = hs.c1;
-          hs.lmsrc = l;
-          hs.qsrc = q;
-          hs.y = y;
+          hs.lmsrc = cl;
+          hs.qsrc = cq;
+          hs.y = cy;
           hs.c1p = c1p;
-          hs.c1 = y != blank ? y : c1p;
+          hs.c1 = cy != blank ? cy : c1p;
         }
       } else {
         // ---- beam: publish this hypothesis' candidates, meet the stream, rank all ----
         int4 *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * 2;
-        const double S0 = hs.S;
-        const int c1_now = hs.c1, fl_now = hs.fl;
-        for (int j = 0; j < K; ++j) {
-          float f;
-          int y, l, q;
-          cand(j, f, y, l, q);
-          if (lane == 0) {
-            if (!act) y = INT_MAX;
-            xs[(b * K + j) * 2] = make_int4(as_int(f), y, l, q);
-            xs[(b * K + j) * 2 + 1] = make_int4(c1_now, fl_now, __double2loint(S0), __double2hiint(S0));
-          }
+        if (lane < K) {
+          const double S0 = hs.S;
+          xs[(b * K + lane) * 2] = make_int4(as_int(cf), act ? cy : INT_MAX, cl, cq);
+          xs[(b * K + lane) * 2 + 1] = make_int4(hs.c1, hs.fl, __double2loint(S0), __double2hiint(S0));
         }
         int *cnt = p.counters + (size_t)sl * kCounterStride;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         if (lane == 0) {
-          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
           __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           const int target = B * (t + 1);
           int spins = 0;
@@ -737,7 +726,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         // every workgroup of the stream ranks the same B*k candidates by
         // (running score + fused desc, parent asc, rank asc); slot b takes rank b
         const int nc = B * K;
-        int hit = 0, rl = 0, rq = 0, ry = 0, rc1 = 0, rfl = 0, rlo = 0, rhi = 0, rpar = 0;
+        int hit = 0, ry = 0, rl = 0, rq = 0, rc1 = 0, rfl = 0, rlo = 0, rhi = 0, rpar = 0;
         for (int i0 = 0; i0 < nc; i0 += 64) {
           const int i = i0 + lane;
           int4 a = make_int4(0, INT_MAX, 0, 0), bb = make_int4(0, 0, 0, 0);
@@ -748,21 +737,28 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           const bool valid = i < nc && a.y != INT_MAX;
           const double sc = valid ? __hiloint2double(bb.w, bb.z) + (double)as_float(a.x) : -INFINITY;
           int r = 0;
-          for (int i2 = 0; i2 < nc; ++i2) {
-            const int src = i2 & 63;
-            // candidates of this 64-block are in registers; others are re-read
-            double sc2;
-            int v2;
-            if ((i2 >> 6) == (i0 >> 6)) {
-              sc2 = __shfl(sc, src);
-              v2 = __shfl((int)valid, src);
-            } else {
-              const int4 a2 = xs[i2 * 2];
-              const int4 b2 = xs[i2 * 2 + 1];
-              v2 = a2.y != INT_MAX;
-              sc2 = __hiloint2double(b2.w, b2.z) + (double)as_float(a2.x);
+          for (int j0 = 0; j0 < nc; j0 += 64) {
+            // candidates of block j0 broadcast by readlane (block i0 is in registers)
+            double scj = sc;
+            int vj = valid;
+            if (j0 != i0) {
+              const int jl = j0 + lane;
+              int4 a2 = make_int4(0, INT_MAX, 0, 0), b2 = make_int4(0, 0, 0, 0);
+              if (jl < nc) {
+                a2 = xs[jl * 2];
+                b2 = xs[jl * 2 + 1];
+              }
+              vj = jl < nc && a2.y != INT_MAX;
+              scj = vj ? __hiloint2double(b2.w, b2.z) + (double)as_float(a2.x) : -INFINITY;
             }
-            if (v2 && (sc2 > sc || (sc2 == sc && i2 < i))) ++r;
+            const int n = min(64, nc - j0);
+            for (int u = 0; u < n; ++u) {
+              const int lo32 = __builtin_amdgcn_readlane(__double2loint(scj), u);
+              const int hi32 = __builtin_amdgcn_readlane(__double2hiint(scj), u);
+              const int vu = __builtin_amdgcn_readlane(vj, u);
+              const double s2 = __hiloint2double(hi32, lo32);
+              if (vu && (s2 > sc || (s2 == sc && j0 + u < i))) ++r;
+            }
           }
           if (valid && r == b) {
             hit = 1;
@@ -780,9 +776,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const int64_t o = (int64_t)t * H + h;
         if (bal) {
           const int src = __ffsll((long long)bal) - 1;
-          const int y = __shfl(ry, src), l = __shfl(rl, src), q = __shfl(rq, src);
-          const int c1p = __shfl(rc1, src), pfl = __shfl(rfl, src);
-          const int slo = __shfl(rlo, src), shi = __shfl(rhi, src), par = __shfl(rpar, src);
+          const int y = __builtin_amdgcn_readlane(ry, src), l = __builtin_amdgcn_readlane(rl, src);
+          const int q = __builtin_amdgcn_readlane(rq, src), c1p = __builtin_amdgcn_readlane(rc1, src);
+          const int pfl = __builtin_amdgcn_readlane(rfl, src), par = __builtin_amdgcn_readlane(rpar, src);
+          const int slo = __builtin_amdgcn_readlane(rlo, src), shi = __builtin_amdgcn_readlane(rhi, src);
           if (lane == 0) {
             hs.lmsrc = l;
             hs.qsrc = q;
