@@ -118,72 +118,54 @@ __device__ __forceinline__ int rec_bo_lane(int L) { return 2 + 3 * (L - 2); }
 __device__ __forceinline__ int rec_beg_lane(int L) { return 3 + 3 * (L - 2); }
 __device__ __forceinline__ int rec_cnt_lane(int L) { return 4 + 3 * (L - 2); }
 
-// sorted per-lane candidate list: key desc, id asc; an entry keeps the token's
-// LDS tag word (LM winner level/offset, phrase transition) so that only the
-// winners resolve where their next state comes from
-template <int KM>
-struct TopK {
-  float k[KM];
-  int y[KM];
-  uint32_t w[KM];
-  __device__ __forceinline__ void init() {
-#pragma unroll
-    for (int i = 0; i < KM; ++i) {
-      k[i] = -INFINITY;
-      y[i] = INT_MAX;
-      w[i] = 0u;
-    }
-  }
-  __device__ __forceinline__ bool wants(float key, int yy) const { return before(key, yy, k[KM - 1], y[KM - 1]); }
-  __device__ __forceinline__ void insert(float key, int yy, uint32_t ww) {
-    k[KM - 1] = key;
-    y[KM - 1] = yy;
-    w[KM - 1] = ww;
-#pragma unroll
-    for (int i = KM - 1; i > 0; --i) {
-      if (before(k[i], y[i], k[i - 1], y[i - 1])) {
-        float tk = k[i]; k[i] = k[i - 1]; k[i - 1] = tk;
-        int ty = y[i]; y[i] = y[i - 1]; y[i - 1] = ty;
-        uint32_t tw = w[i]; w[i] = w[i - 1]; w[i - 1] = tw;
-      }
-    }
-  }
-  __device__ __forceinline__ void pop() {
-#pragma unroll
-    for (int i = 0; i < KM - 1; ++i) {
-      k[i] = k[i + 1];
-      y[i] = y[i + 1];
-      w[i] = w[i + 1];
-    }
-    k[KM - 1] = -INFINITY;
-    y[KM - 1] = INT_MAX;
-  }
-};
-
-// ---- wave-level argmax over (key desc, id asc) with DPP moves (no LDS) --------
+// ---- wave-level reductions with DPP moves (no LDS) ------------------------------
+// rows of 16 lanes: quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror,
+// row_mirror; then row_bcast:15 (rows 1, 3) and row_bcast:31 (rows 2, 3) carry
+// the row results to lane 63
 template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_f(float ident, float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(ident), __float_as_int(v), CTRL, ROWS, 0xF, false));
+}
+__device__ __forceinline__ float row_max(float v) {
+  v = fmaxf(v, dpp_f<0xB1, 0xF>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x4E, 0xF>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x141, 0xF>(-INFINITY, v));
+  return fmaxf(v, dpp_f<0x140, 0xF>(-INFINITY, v));
+}
+__device__ __forceinline__ float row_sum(float v) {
+  v = v + dpp_f<0xB1, 0xF>(0.0f, v);
+  v = v + dpp_f<0x4E, 0xF>(0.0f, v);
+  v = v + dpp_f<0x141, 0xF>(0.0f, v);
+  return v + dpp_f<0x140, 0xF>(0.0f, v);
+}
+// uniform maximum / sum over the wave
+__device__ __forceinline__ float wave_max(float v) {
+  v = row_max(v);
+  v = fmaxf(v, dpp_f<0x142, 0xA>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x143, 0xC>(-INFINITY, v));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v = row_sum(v);
+  v = v + dpp_f<0x142, 0xA>(0.0f, v);
+  v = v + dpp_f<0x143, 0xC>(0.0f, v);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+// every lane of each 16-lane row ends with the row's best (key desc, id asc)
+template <int CTRL>
 __device__ __forceinline__ void dpp_best(float &k, int &y) {
-  const float k2 = __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(-INFINITY), __float_as_int(k), CTRL, ROWS, 0xF, false));
-  const int y2 = __builtin_amdgcn_update_dpp(INT_MAX, y, CTRL, ROWS, 0xF, false);
+  const float k2 = dpp_f<CTRL, 0xF>(-INFINITY, k);
+  const int y2 = __builtin_amdgcn_update_dpp(INT_MAX, y, CTRL, 0xF, 0xF, false);
   if (before(k2, y2, k, y)) {
     k = k2;
     y = y2;
   }
 }
-// every lane of each 16-lane row ends with the row's best
 __device__ __forceinline__ void row_best(float &k, int &y) {
-  dpp_best<0xB1, 0xF>(k, y);   // quad_perm [1,0,3,2]
-  dpp_best<0x4E, 0xF>(k, y);   // quad_perm [2,3,0,1]
-  dpp_best<0x141, 0xF>(k, y);  // row_half_mirror
-  dpp_best<0x140, 0xF>(k, y);  // row_mirror
-}
-// the wave's best, returned uniformly (lane 63 holds it after the row broadcasts)
-__device__ __forceinline__ void wave_best(float k, int y, float &bk, int &by) {
-  row_best(k, y);
-  dpp_best<0x142, 0xA>(k, y);  // row_bcast:15 -> rows 1, 3
-  dpp_best<0x143, 0xC>(k, y);  // row_bcast:31 -> rows 2, 3
-  bk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(k), 63));
-  by = __builtin_amdgcn_readlane(y, 63);
+  dpp_best<0xB1>(k, y);
+  dpp_best<0x4E>(k, y);
+  dpp_best<0x141>(k, y);
+  dpp_best<0x140>(k, y);
 }
 
 // hypothesis state carried between frames (LDS, written by one lane)
@@ -207,11 +189,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   float *sE = reinterpret_cast<float *>(dyn) + 2 * Vp;
   int *sDT = reinterpret_cast<int *>(sE + kAux);
   int *sTN = sDT + kAux;
-  __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves], s_pax[kMaxWaves];
+  __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves];
   __shared__ int s_paid[kMaxWaves];
   __shared__ float w_key[kMaxWaves][KM];
   __shared__ int w_y[kMaxWaves][KM];
-  __shared__ uint32_t w_tag[kMaxWaves][KM];
   __shared__ HypState hs;
   __shared__ const int2 *s_arcs[kMaxLevels];
   __shared__ long long s_sbase[kMaxLevels];
@@ -291,6 +272,12 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const bool act = (fl & 1) != 0;
     const bool inv = act && (fl & 2) != 0;
     const bool ok = act && !inv;
+    // the tag words of the previous frame (its winners read them before its last
+    // barrier) are cleared before this frame's scatter
+    if (t > 0) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c) *reinterpret_cast<uint4 *>(win + (c * W + g) * 4) = make_uint4(0u, 0u, 0u, 0u);
+    }
     const int lmsrc = uni(hs.lmsrc), qsrc = uni(hs.qsrc), yin = uni(hs.y);
     int c1 = uni(hs.c1);
     // ---- hop 1: state record, phrase node, logits row ------------------------------
@@ -352,7 +339,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const int dbeg = has_node ? rdl(rw, kNodeLane + 1) : 0;
     const int dcnt = has_node ? rdl(rw, kNodeLane + 2) : 0;
     const int qid = has_node ? rdl(rw, kNodeLane + 3) : qsrc;
-    // backoffs of levels 2..7, +0.0 above m (an exact no-op on the sums)
+    // backoffs of levels 2..m (0 above m, never added)
     float bo[kMaxLevels];
 #pragma unroll
     for (int L = 2; L < kMaxLevels; ++L) bo[L] = (L <= m) ? as_float(rdl(rw, rec_bo_lane(L))) : 0.0f;
@@ -398,47 +385,43 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       dd[u] = make_int4(INT_MAX, 0, 0, 0);
       if (j < dcnt) dd[u] = tr.delta[dbeg + j];
     }
-    // ---- row statistics: online max / sum-exp and raw argmax --------------------
+    // ---- row statistics: wave max, sum of exp below it, raw argmax ----------------
     {
-      float lmx = -INFINITY, ax = -INFINITY, lsum = 0.0f;
+      float lmx = -INFINITY;
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) lmx = fmaxf(lmx, xv[c][j]);
+      const float mw = wave_max(lmx);
+      float lsum = 0.0f;
+      if (mw > -INFINITY) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) lsum += (xv[c][j] > -INFINITY) ? expf(xv[c][j] - mw) : 0.0f;
+      }
+      const float sw = wave_sum(lsum);
+      // lowest id holding the wave max (only the acoustic blank decision needs it)
       int aid = INT_MAX;
+      if (p.mode == FUSION_BLANK_AM && mw > -INFINITY) {
 #pragma unroll
-      for (int c = 0; c < NC; ++c)
+        for (int c = NC - 1; c >= 0; --c) {
+          unsigned long long mj[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int y = (c * W + g) * 4 + j;
-          const float x = xv[c][j];
-          lmx = fmaxf(lmx, x);
-          if (x > ax) {
-            ax = x;
-            aid = y;
+          for (int j = 0; j < 4; ++j) mj[j] = __ballot(xv[c][j] == mw && (c * W + g) * 4 + j < V);
+          const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
+          if (any) {
+            const int src = __ffsll((long long)any) - 1;
+            int jj = 3;
+#pragma unroll
+            for (int j = 2; j >= 0; --j) jj = ((mj[j] >> src) & 1ull) ? j : jj;
+            aid = (c * W + wave * 64 + src) * 4 + jj;
           }
-        }
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (xv[c][j] > -INFINITY) lsum += expf(xv[c][j] - lmx);
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        const float om = __shfl_xor(lmx, off);
-        const float os = __shfl_xor(lsum, off);
-        const float oax = __shfl_xor(ax, off);
-        const int oaid = __shfl_xor(aid, off);
-        const float nm = fmaxf(lmx, om);
-        const float a = (lmx > -INFINITY) ? lsum * expf(lmx - nm) : 0.0f;
-        const float bb = (om > -INFINITY) ? os * expf(om - nm) : 0.0f;
-        lmx = nm;
-        lsum = a + bb;
-        if (oax > ax || (oax == ax && oaid < aid)) {
-          ax = oax;
-          aid = oaid;
         }
       }
       if (lane == 0) {
-        s_pm[wave] = lmx;
-        s_ps[wave] = lsum;
-        s_pax[wave] = ax;
+        s_pm[wave] = mw;
+        s_ps[wave] = sw;
         s_paid[wave] = aid;
       }
     }
@@ -460,7 +443,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         float v = as_float(a.y);
 #pragma unroll
         for (int L2 = 3; L2 < kMaxLevels; ++L2)
-          if (L2 > L) v = v + bo[L2];
+          if (L2 > L && L2 <= m) v = v + bo[L2];
         lmval[y] = v;
         win16[2 * y] = (uint16_t)((L << 13) | j);
         if (L == N - 1 && j < kAux) sTN[j] = tnext;
@@ -517,85 +500,115 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
       __syncthreads();
     }
-    // ---- keys, fused row, per-lane top-k, clear of the owned LDS entries --------
-    float M = -INFINITY, amx = -INFINITY, Ssum = 0.0f;
-    int am = INT_MAX;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, s_pm[w]);
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      if (s_pm[w] > -INFINITY) Ssum += s_ps[w] * expf(s_pm[w] - M);
-      if (s_pax[w] > amx || (s_pax[w] == amx && s_paid[w] < am)) {
-        amx = s_pax[w];
-        am = s_paid[w];
+    // ---- combine the row statistics (lanes 0..NW-1 hold one wave each) --------------
+    float lse;
+    int am;
+    {
+      const bool wl = lane < NW;
+      const float pm = wl ? s_pm[lane] : -INFINITY;
+      const float M = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_max(pm)), 0));
+      const float term = (wl && pm > -INFINITY) ? s_ps[lane] * expf(pm - M) : 0.0f;
+      lse = M + logf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_sum(term)), 0)));
+      am = INT_MAX;
+      if (p.mode == FUSION_BLANK_AM) {
+        float ak = pm;
+        int ay = wl ? s_paid[lane] : INT_MAX;
+        row_best(ak, ay);
+        am = __builtin_amdgcn_readlane(ay, 0);
       }
     }
-    const float lse = M + logf(Ssum);
+    // ---- keys and the fused row ------------------------------------------------------
     const bool blank_only = inv || (p.mode == FUSION_BLANK_AM && am == blank);
     const bool want_keys = ok && (!blank_only || p.fused);
     const bool write_fused = p.fused != nullptr && ok;
     const rsrc_t fr = row_rsrc(write_fused ? p.fused + rowoff : p.logits, write_fused ? V : 0);
-    TopK<KM> tk;
-    tk.init();
+    float kk[NC][4];
+    uint32_t vm = 0u;  // bit c*4+j: token (c, j) of this lane is still a candidate
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int y0 = (c * W + g) * 4;
-      const uint4 w4 = *reinterpret_cast<const uint4 *>(win + y0);
-      const float4 l4 = *reinterpret_cast<const float4 *>(lmval + y0);
-      const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
-      const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-      float kk[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int y = y0 + j;
-        const float x = xv[c][j];
-        const uint32_t lo = ww[j] & 0xFFFFu, hi = ww[j] >> 16;
-        // LM: the scattered value if an arc won, else the dense row plus the
-        // backoffs of levels 2.. (the +0.0 terms above m change nothing)
-        float dres = lv[j];
-#pragma unroll
-        for (int L2 = 2; L2 < kMaxLevels; ++L2) dres = dres + bo[L2];
-        const float lmv = lo ? lv[j] : dres;
-        // phrases: the transition's entry value if this state overrides y, else the root's
-        const int hidx = hi ? min((int)hi - 1, kAux - 1) : 0;
-        float e = hi ? sE[hidx] : rE[c][j];
-        if ((int)hi > kAux) e = as_float(tr.delta[dbeg + (int)hi - 1].z);
-        const float bst = e - phiq;
-        const float a1 = p.lam * lmv;
-        const float a2 = x + a1;
-        const float a3 = p.beta * (p.has_trie ? bst : 0.0f);
-        const float key = (y == blank) ? x : a2 + a3;
-        kk[j] = key;
-        const bool live_tok = act && y < V;
-        if (live_tok && blank_only && y == blank) tk.insert(x, blank, 0u);
-        if (live_tok && want_keys && !blank_only && (p.mode == FUSION_BLANK_COMPETE || y != blank) &&
-            tk.wants(key, y))
-          tk.insert(key, y, ww[j]);
+        const bool cand = act && y < V && (blank_only ? y == blank : (p.mode == FUSION_BLANK_COMPETE || y != blank));
+        vm |= cand ? (1u << (c * 4 + j)) : 0u;
+        kk[c][j] = xv[c][j];
       }
-      *reinterpret_cast<uint4 *>(win + y0) = make_uint4(0u, 0u, 0u, 0u);
+      if (want_keys) {
+        const uint4 w4 = *reinterpret_cast<const uint4 *>(win + y0);
+        const float4 l4 = *reinterpret_cast<const float4 *>(lmval + y0);
+        const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
+        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int y = y0 + j;
+          const float x = xv[c][j];
+          const uint32_t lo = ww[j] & 0xFFFFu, hi = ww[j] >> 16;
+          // LM: the scattered value if an arc won, else the dense row plus the
+          // backoffs of levels 2..m in increasing order
+          float dres = lv[j];
+#pragma unroll
+          for (int L2 = 2; L2 < kMaxLevels; ++L2)
+            if (L2 <= m) dres = dres + bo[L2];
+          const float lmv = lo ? lv[j] : dres;
+          // phrases: the transition's entry value if this state overrides y, else the root's
+          const int hidx = hi ? min((int)hi - 1, kAux - 1) : 0;
+          float e = hi ? sE[hidx] : rE[c][j];
+          if ((int)hi > kAux) e = as_float(tr.delta[dbeg + (int)hi - 1].z);
+          const float bst = e - phiq;
+          const float a1 = p.lam * lmv;
+          const float a2 = x + a1;
+          const float a3 = p.beta * (p.has_trie ? bst : 0.0f);
+          kk[c][j] = (y == blank) ? x : a2 + a3;
+        }
+      }
       if (write_fused && y0 < V) {
         if (AL) {
-          row_store4(fr, make_float4(kk[0] - lse, kk[1] - lse, kk[2] - lse, kk[3] - lse), voff, c * W * 16);
+          row_store4(fr, make_float4(kk[c][0] - lse, kk[c][1] - lse, kk[c][2] - lse, kk[c][3] - lse), voff, c * W * 16);
         } else {
 #pragma unroll
           for (int j = 0; j < 4; ++j)
-            if (y0 + j < V) row_store1(fr, kk[j] - lse, voff + 4 * j, c * W * 16);
+            if (y0 + j < V) row_store1(fr, kk[c][j] - lse, voff + 4 * j, c * W * 16);
         }
       }
     }
-    // ---- wave top-k (DPP argmax, K rounds); the owning lane writes each winner -----
-    for (int j = 0; j < K; ++j) {
-      float bk;
-      int by;
-      wave_best(tk.k[0], tk.y[0], bk, by);
-      if (by == INT_MAX) {
-        if (lane == 0) w_y[wave][j] = INT_MAX;
-      } else if (tk.y[0] == by) {
-        w_key[wave][j] = bk;
-        w_y[wave][j] = by;
-        w_tag[wave][j] = tk.w[0];
-        tk.pop();
+    // ---- the wave's top-k: per round the wave maximum of the remaining keys, then
+    // the lowest id holding it (ties to the lowest id); uniform values throughout --
+    {
+      int r = 0;
+      for (; r < K; ++r) {
+        float lb = -INFINITY;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) lb = ((vm >> (c * 4 + j)) & 1u) ? fmaxf(lb, kk[c][j]) : lb;
+        const float M = wave_max(lb);
+        int wy = INT_MAX, wsrc = 0, wbit = 0;
+#pragma unroll
+        for (int c = NC - 1; c >= 0; --c) {
+          unsigned long long mj[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) mj[j] = __ballot(((vm >> (c * 4 + j)) & 1u) && kk[c][j] == M);
+          const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
+          if (any) {
+            const int src = __ffsll((long long)any) - 1;
+            int jj = 3;
+#pragma unroll
+            for (int j = 2; j >= 0; --j) jj = ((mj[j] >> src) & 1ull) ? j : jj;
+            wy = (c * W + wave * 64 + src) * 4 + jj;
+            wsrc = src;
+            wbit = c * 4 + jj;
+          }
+        }
+        if (wy == INT_MAX) break;
+        if (lane == 0) {
+          w_key[wave][r] = M;
+          w_y[wave][r] = wy;
+        }
+        if (lane == wsrc) vm &= ~(1u << wbit);
       }
+      if (lane == 0)
+        for (; r < K; ++r) w_y[wave][r] = INT_MAX;
     }
     if (p.traffic && act && g == 0) {
       unsigned long long by = 4ull * V;
@@ -617,18 +630,15 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       // lane w < NW holds wave w's list (best first)
       float hk[KM];
       int hy[KM];
-      uint32_t hw[KM];
 #pragma unroll
       for (int j = 0; j < KM; ++j) {
         const bool have = lane < NW && j < K;
         hy[j] = have ? w_y[lane][j] : INT_MAX;
         hk[j] = (have && hy[j] != INT_MAX) ? w_key[lane][j] : -INFINITY;
-        hw[j] = have ? w_tag[lane][j] : 0u;
       }
       // candidate j ends in lane j
       float ck = -INFINITY;
       int cy = INT_MAX;
-      uint32_t cw = 0u;
       for (int j = 0; j < K; ++j) {
         float k = hk[0];
         int y = hy[0];
@@ -638,18 +648,15 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         if (by == INT_MAX) break;
         const unsigned long long own = __ballot(hy[0] == by && lane < NW);
         const int src = __ffsll((long long)own) - 1;
-        const uint32_t wsrc = (uint32_t)__builtin_amdgcn_readlane((int)hw[0], src);
         if (lane == j) {
           ck = bk;
           cy = by;
-          cw = wsrc;
         }
         if (lane == src) {
 #pragma unroll
           for (int i = 0; i < KM - 1; ++i) {
             hk[i] = hk[i + 1];
             hy[i] = hy[i + 1];
-            hw[i] = hw[i + 1];
           }
           hk[KM - 1] = -INFINITY;
           hy[KM - 1] = INT_MAX;
@@ -659,6 +666,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       const float cf = ck - lse;
       int cl = sid, cq = qid;
       if (cy != INT_MAX && cy != blank) {
+        // the token's LDS tag word: LM winner level / offset, phrase transition
+        const uint32_t cw = win[cy];
         const uint32_t lo = cw & 0xFFFFu, hi = cw >> 16;
         cl = -1;
         if (lo) {
