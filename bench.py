@@ -14,8 +14,10 @@ same workload, whose decisions are also checked against the GPU trajectory.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -32,6 +34,46 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+# sources that decide what the fusion kernel reads and writes; the HBM traffic
+# recorded under profiles/ is reported only while they are unchanged
+KERNEL_SOURCES = ("paper_2609_14991_amd/csrc/fusion_kernels.hip", "paper_2609_14991_amd/csrc/fusion_internal.h",
+                  "paper_2609_14991_amd/csrc/ngram_tables.cpp", "paper_2609_14991_amd/csrc/boost_trie.cpp")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fusion_kernel_c5_hbm_traffic.md")
+
+
+def kernel_sources_digest():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(workload):
+    """(bytes per launch, source digest) from the committed PMC summary, or None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    txt = open(TRAFFIC_FILE).read()
+    fields = dict(re.findall(r"^- (\w+): `([^`]*)`", txt, re.M))
+    if fields.get("workload") != workload or "traffic_bytes_per_launch" not in fields:
+        return None
+    return int(float(fields["traffic_bytes_per_launch"])), fields.get("kernel_sources_digest")
+
+
+def copy_probe(nbytes):
+    """A plain device copy of known size, for scaling the FETCH_SIZE / WRITE_SIZE counters."""
+    import torch
+
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"copied {n * 4} bytes 3 times")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -40,9 +82,14 @@ def main():
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--fused", action="store_true", help="also write the full fused score rows")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
-    ap.add_argument("--cpu-frames", type=int, default=12)
-    ap.add_argument("--cpu-streams", type=int, default=16)
+    ap.add_argument("--cpu-frames", type=int, default=300)
+    ap.add_argument("--cpu-streams", type=int, default=64)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device copy of this size (counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
               "(the fusion path shards by stream with no per-step exchange; see DESIGN.md)",
@@ -153,6 +200,7 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": None,
+            "traffic_note": None,
             "algorithmic_bytes_per_launch": alg_bytes,
             "bytes_per_hyp_step": alg_bytes / max(hyp_steps, 1),
             "hyp_steps_per_launch": hyp_steps,
@@ -160,6 +208,18 @@ def main():
         },
         "cpu_baseline": None,
     }
+    rec = recorded_traffic(w.name)
+    digest = kernel_sources_digest()
+    if rec is None:
+        out["roofline"]["traffic_note"] = "no PMC record for this workload under profiles/"
+    elif rec[1] != digest:
+        out["roofline"]["traffic_note"] = f"PMC record is for kernel sources {rec[1]}, these are {digest}"
+    elif args.fused:
+        out["roofline"]["traffic_note"] = "PMC record is for the run without fused rows"
+    else:
+        out["roofline"]["traffic"] = rec[0]
+        out["roofline"]["traffic_note"] = ("HBM bytes per launch: rocprofv3 FETCH_SIZE + WRITE_SIZE, each scaled "
+                                           "by the counter's reading for a plain copy of known size")
 
     if not args.no_cpu:
         import oracle
