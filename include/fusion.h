@@ -187,6 +187,24 @@ int fusion_run(const NgramTables *lm, const BoostTrie *trie, const float *logits
                double *hyp_score, int32_t *tokens, int32_t *parents, float *fused,
                int64_t *traffic, hipStream_t stream);
 
+/*
+ * joint_project - output projection of the Transducer joint network (the
+ * network whose log-softmax is the acoustic term of Eq. (1), Sec. III-C),
+ * for M hypothesis-frames at once, on the matrix cores:
+ *     out[m, n] = sum_k A[m, k] * W[n, k] + bias[n]
+ *   A      device [M, K] bf16 (raw 16-bit patterns), row-major: joint hidden states
+ *   W      device [N, K] bf16, row-major (a linear layer's weight, N = vocabulary)
+ *   bias   device [N] fp32 or NULL
+ *   out    device [M, N] fp32, row-major: the logits fusion_step / fusion_run read
+ * Products are exact in fp32; the K products of an output are summed in fp32
+ * in an unspecified order, then the bias is added.  M >= 0 (0 does nothing),
+ * N >= 1, K >= 8 with K % 8 == 0 (FUSION_E_UNSUPPORTED otherwise), A and W
+ * 16-byte aligned, each operand under 2 GiB (split larger calls along M).
+ * All buffers belong to the caller; the call only enqueues work on `stream`.
+ */
+int joint_project(const uint16_t *A, const uint16_t *W, const float *bias, int32_t M, int32_t N,
+                  int32_t K, float *out, hipStream_t stream);
+
 /* description of the calling thread's last failure (library-owned string) */
 const char *fusion_last_error(void);
 /* synchronizes `stream`, returns the device status bits in *code and clears them */

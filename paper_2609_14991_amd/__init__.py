@@ -31,7 +31,8 @@ FUSION_STATUS_BAD_LM_STATE = 1
 FUSION_STATUS_BAD_BOOST_STATE = 2
 
 EXPORTS = ("ngram_load", "ngram_bos_state", "ngram_info", "ngram_free", "boost_build", "boost_info",
-           "boost_free", "fusion_step", "fusion_run", "fusion_last_error", "fusion_device_status")
+           "boost_free", "fusion_step", "fusion_run", "joint_project", "fusion_last_error",
+           "fusion_device_status")
 
 
 class FusionError(RuntimeError):
@@ -73,6 +74,8 @@ def lib():
         L.fusion_run.restype = ctypes.c_int
         L.fusion_run.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, f32, f32, i32, i32, vp, vp, vp,
                                  vp, vp, vp, vp, vp]
+        L.joint_project.restype = ctypes.c_int
+        L.joint_project.argtypes = [vp, vp, vp, i32, i32, i32, vp, vp]
         L.fusion_last_error.restype = ctypes.c_char_p
         L.fusion_last_error.argtypes = []
         L.fusion_device_status.restype = ctypes.c_int
@@ -214,6 +217,13 @@ def fusion_run(lm, trie, logits, T, S, B, V, k, lam, beta, blank_id, blank_mode,
                             _ptr(fused), _ptr(traffic), _stream(stream)))
 
 
+def joint_project(A, W, bias, M, N, K, out, stream=None):
+    """Same arguments as the C call; A and W are int16/uint16 (bf16 bit patterns) or
+    bfloat16 CUDA tensors, bias and out float32 CUDA tensors."""
+    _check(lib().joint_project(_ptr(A), _ptr(W), _ptr(bias), int(M), int(N), int(K), _ptr(out),
+                               _stream(stream)))
+
+
 def fusion_device_status(stream=None) -> int:
     v = ctypes.c_int32()
     _check(lib().fusion_device_status(_stream(stream), ctypes.byref(v)))
@@ -238,6 +248,17 @@ def step(lm, trie, logits, lm_state, boost_state, lam, beta, blank_id, k, blank_
     )
     fusion_step(lm, trie, logits, lm_state, boost_state, H, V, lam, beta, blank_id, k, blank_mode,
                 out["fused"], out["tokens"], out["scores"], out["next_lm"], out["next_boost"], stream)
+    return out
+
+
+def project(A, W, bias=None, stream=None):
+    """logits [M, N] fp32 of A [M, K] and W [N, K] (bf16 CUDA tensors)."""
+    import torch
+
+    M, K = A.shape
+    N = W.shape[0]
+    out = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    joint_project(A, W, bias, M, N, K, out, stream)
     return out
 
 

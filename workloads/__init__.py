@@ -16,6 +16,8 @@ from .gen import (  # noqa: F401
     estimate_kn,
     make_phrases,
     make_logits,
+    make_projection,
+    to_bf16_bits,
     load_workload,
     tiny_random_lm,
     tiny_random_phrases,

@@ -354,6 +354,29 @@ def make_logits(rng, T: int, H: int, V: int, blank: int = 0, sigma: float = 2.0,
 # --------------------------------------------------------------------------
 # workload assembly
 # --------------------------------------------------------------------------
+def to_bf16_bits(x) -> np.ndarray:
+    """float32 values -> bfloat16 bit patterns (uint16), rounded to nearest even.
+    Input encoding only (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    return ((u + (np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1)))) >> np.uint32(16)).astype(np.uint16)
+
+
+def make_projection(cfg: int = 5, M: int | None = None, K: int = 640, N: int | None = None,
+                    blank: int = 0):
+    """Inputs of the joint output projection: hidden states A ~ N(0, 1) [M, K]
+    and weight W ~ N(0, (2 / sqrt(K))^2) [N, K] as bf16 bit patterns, fp32 bias
+    N(0, 0.1^2) with +2 on blank.  M defaults to T * H of the config, N to V."""
+    c = CONFIGS[cfg]
+    M = c["T"] * c["S"] * c["B"] if M is None else int(M)
+    N = c["V"] if N is None else int(N)
+    r = seed_streams(cfg)[4]
+    A = to_bf16_bits(r.standard_normal((M, K), dtype=np.float32))
+    W = to_bf16_bits(r.standard_normal((N, K), dtype=np.float32) * np.float32(2.0 / np.sqrt(K)))
+    bias = (r.standard_normal(N, dtype=np.float32) * np.float32(0.1)).astype(np.float32)
+    bias[blank] += np.float32(2.0)
+    return A, W, bias
+
+
 @functools.lru_cache(maxsize=2)
 def _corpus_and_lm(lm_seed: int):
     c = CONFIGS[lm_seed]
