@@ -33,8 +33,9 @@ struct LMDevice {
   const int32_t *rec_dense = nullptr;  // [(V+2) * V * rec_stride]  record of the state after (w, y)
   const int32_t *cnt1 = nullptr;       // [V+2]        explicit bigram successors with y < V
   const int32_t *rec = nullptr;        // [(n_states - (V+2)) * rec_stride] state records
-  const int2 *arcs[FUSION_MAX_ORDER] = {};  // arcs[L], L = 2..N-1: (token, logp bits) of order L+1
-  const int32_t *top_next = nullptr;   // [n_N]  state after an order-N arc
+  const int2 *arcs = nullptr;          // (token, logp bits) of the arcs of levels 2..N-1, level by level
+  int64_t arc_base[FUSION_MAX_ORDER] = {};  // first arc of level L (arcs of order L+1 n-grams)
+  const int32_t *top_next = nullptr;   // [n_N]  state after an order-N arc (index - arc_base[N-1])
   int64_t off[FUSION_MAX_ORDER + 2] = {};   // off[k] = first id of order-k states (k >= 2)
   int64_t n_states = 0;
   int32_t N = 0, V = 0, blank = 0, rec_stride = 0, eos_ok = 0, pad = 0;
@@ -44,7 +45,7 @@ struct LMDevice {
 //   [0]                     c_1 | (m << 16)
 //   [1]                     state id
 //   [2 + 3*(L-2) + 0]       bo(c_L) as float bits      (L = 2..m)
-//   [2 + 3*(L-2) + 1]       first arc of c_L in arcs[L]
+//   [2 + 3*(L-2) + 1]       first arc of c_L (index into arcs)
 //   [2 + 3*(L-2) + 2]       number of arcs of c_L
 // (a one-token state w has m = 1 and no level entries)
 inline int record_stride(int N) {

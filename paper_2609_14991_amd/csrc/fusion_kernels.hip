@@ -85,7 +85,6 @@ __device__ __forceinline__ bool before(float ka, int ya, float kb, int yb) {
   return ka > kb || (ka == kb && ya < yb);
 }
 __device__ __forceinline__ float as_float(int v) { return __int_as_float(v); }
-__device__ __forceinline__ int as_int(float v) { return __float_as_int(v); }
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ int rdl(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 __device__ __forceinline__ unsigned long long umin64(unsigned long long a, unsigned long long b) {
@@ -138,19 +137,38 @@ __device__ __forceinline__ float row_sum(float v) {
   v = v + dpp_f<0x141, 0xF>(0.0f, v);
   return v + dpp_f<0x140, 0xF>(0.0f, v);
 }
-// uniform maximum / sum over the wave
-__device__ __forceinline__ float wave_max(float v) {
-  v = row_max(v);
-  v = fmaxf(v, dpp_f<0x142, 0xA>(-INFINITY, v));
-  v = fmaxf(v, dpp_f<0x143, 0xC>(-INFINITY, v));
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
+// uniform sum over the wave
 __device__ __forceinline__ float wave_sum(float v) {
   v = row_sum(v);
   v = v + dpp_f<0x142, 0xA>(0.0f, v);
   v = v + dpp_f<0x143, 0xC>(0.0f, v);
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
+// order-preserving map of non-NaN floats onto int32 (x + 0.0 first folds -0
+// into +0, so equal floats map to equal ints); an involution
+__device__ __forceinline__ int ord_key(float x) {
+  const int b = __float_as_int(x + 0.0f);
+  return b ^ ((b >> 31) & 0x7FFFFFFF);
+}
+__device__ __forceinline__ float key_of(int i) { return __int_as_float(i ^ ((i >> 31) & 0x7FFFFFFF)); }
+// uniform maximum of an int over the wave (identity INT_MIN)
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(INT_MIN, v, CTRL, ROWS, 0xF, false);
+}
+__device__ __forceinline__ int wave_max_i(int v) {
+  v = max(v, dpp_i<0xB1, 0xF>(v));
+  v = max(v, dpp_i<0x4E, 0xF>(v));
+  v = max(v, dpp_i<0x141, 0xF>(v));
+  v = max(v, dpp_i<0x140, 0xF>(v));
+  v = max(v, dpp_i<0x142, 0xA>(v));
+  v = max(v, dpp_i<0x143, 0xC>(v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+// e^x through the hardware base-2 exponential (about 1e-6 relative error near
+// the arguments used here, x <= 0)
+__device__ __forceinline__ float exp_fast(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+
 // every lane of each 16-lane row ends with the row's best (key desc, id asc)
 template <int CTRL>
 __device__ __forceinline__ void dpp_best(float &k, int &y) {
@@ -191,11 +209,14 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   int *sTN = sDT + kAux;
   __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves];
   __shared__ int s_paid[kMaxWaves];
-  __shared__ float w_key[kMaxWaves][KM];
+  __shared__ int w_key[kMaxWaves][KM];  // order-preserving images of the keys (ord_key)
   __shared__ int w_y[kMaxWaves][KM];
   __shared__ HypState hs;
-  __shared__ const int2 *s_arcs[kMaxLevels];
-  __shared__ long long s_sbase[kMaxLevels];
+  // beam rendezvous staging (wave 0): candidate records, parent flags, totals
+  __shared__ int4 s_xa[FUSION_MAX_BEAM * FUSION_MAX_K];
+  __shared__ int s_xf[FUSION_MAX_BEAM * FUSION_MAX_K];
+  __shared__ double s_tot[FUSION_MAX_BEAM * FUSION_MAX_K];
+  __shared__ long long s_sbase[kMaxLevels];  // state id of arc index i of level L < N-1: s_sbase[L] + i
   __shared__ int s_lbeg[kMaxLevels];  // first arc of each level of the current state
   __shared__ int s_cfg[2];  // V, blank: re-read each frame so per-token masks stay inside the loop
   __shared__ unsigned long long s_bytes, s_steps;
@@ -228,8 +249,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 
   // ---- prologue ------------------------------------------------------------------
   if (g < kMaxLevels) {
-    s_arcs[g] = lm.arcs[g];
-    s_sbase[g] = (g >= 2 && g + 1 <= N - 1) ? lm.off[g + 1] : -1;
+    s_sbase[g] = (g >= 2 && g + 1 <= N - 1) ? lm.off[g + 1] - lm.arc_base[g] : 0;
   }
   if (g == 0) {
     s_cfg[0] = p.V;
@@ -332,29 +352,28 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
     }
     // ---- decode the record ------------------------------------------------------
+    // (words a record does not use, the levels above m among them, read as 0, as do
+    // the node lanes without a node)
     const int m = rp ? (rdl(rw, 0) >> 16) : 1;
     const int sid = rp ? rdl(rw, 1) : lmsrc;
-    const bool has_node = np != nullptr;
-    const float phiq = has_node ? as_float(rdl(rw, kNodeLane)) : 0.0f;
-    const int dbeg = has_node ? rdl(rw, kNodeLane + 1) : 0;
-    const int dcnt = has_node ? rdl(rw, kNodeLane + 2) : 0;
-    const int qid = has_node ? rdl(rw, kNodeLane + 3) : qsrc;
-    // backoffs of levels 2..m (0 above m, never added)
+    const float phiq = as_float(rdl(rw, kNodeLane));
+    const int dbeg = rdl(rw, kNodeLane + 1);
+    const int dcnt = rdl(rw, kNodeLane + 2);
+    const int qid = np ? rdl(rw, kNodeLane + 3) : qsrc;
+    // backoffs, first arcs and arc counts of levels 2..7 as uniform values
+    // (readlane at fixed lanes is valid whatever the active mask); adding the
+    // zero backoffs above m changes no sum (at most the sign of a zero)
     float bo[kMaxLevels];
-#pragma unroll
-    for (int L = 2; L < kMaxLevels; ++L) bo[L] = (L <= m) ? as_float(rdl(rw, rec_bo_lane(L))) : 0.0f;
-    // ---- hop 2: first arcs of levels 2..m (flattened) and first phrase transitions --
-    int total_arcs = 0;
-    for (int L = 2; L <= m; ++L) total_arcs += rdl(rw, rec_cnt_lane(L));
-    if (!ok) total_arcs = 0;
-    // per-level counts and first arcs as uniform values (readlane at fixed
-    // lanes is valid whatever the active mask)
     int lcnt[kMaxLevels], lbeg[kMaxLevels];
+    int total_arcs = 0;
 #pragma unroll
     for (int L = 2; L < kMaxLevels; ++L) {
-      lcnt[L] = (L <= m) ? rdl(rw, rec_cnt_lane(L)) : 0;
-      lbeg[L] = (L <= m) ? rdl(rw, rec_beg_lane(L)) : 0;
+      bo[L] = as_float(rdl(rw, rec_bo_lane(L)));
+      lcnt[L] = rdl(rw, rec_cnt_lane(L));
+      lbeg[L] = rdl(rw, rec_beg_lane(L));
+      total_arcs += lcnt[L];
     }
+    // ---- hop 2: first arcs of levels 2..m (flattened) and first phrase transitions --
     int2 ab[kUA];
     int at[kUA], tn[kUA];  // at = level << 16 | offset within the level
 #pragma unroll
@@ -367,15 +386,15 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       int L = 2, bL = lbeg[2];
 #pragma unroll
       for (int L2 = 2; L2 < kMaxLevels - 1; ++L2) {
-        const bool past = (L == L2) && (f >= lcnt[L2]) && (L2 < m);
+        const bool past = (L == L2) && (f >= lcnt[L2]);
         f = past ? f - lcnt[L2] : f;
         L = past ? L2 + 1 : L;
         bL = past ? lbeg[L2 + 1] : bL;
       }
       if (u * W + g < total_arcs) {
         at[u] = (L << 16) | f;
-        ab[u] = s_arcs[L][bL + f];
-        if (L == N - 1 && f < kAux) tn[u] = lm.top_next[bL + f];
+        ab[u] = lm.arcs[bL + f];
+        if (L == N - 1 && f < kAux) tn[u] = lm.top_next[bL + f - lm.arc_base[N - 1]];
       }
     }
     int4 dd[kUD];
@@ -387,18 +406,23 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     }
     // ---- row statistics: wave max, sum of exp below it, raw argmax ----------------
     {
-      float lmx = -INFINITY;
+      int xo[NC][4];  // order-preserving images of the logits (excluded tokens: -inf)
+      int lmx = INT_MIN;
 #pragma unroll
       for (int c = 0; c < NC; ++c)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) lmx = fmaxf(lmx, xv[c][j]);
-      const float mw = wave_max(lmx);
+        for (int j = 0; j < 4; ++j) {
+          xo[c][j] = ord_key(xv[c][j]);
+          lmx = max(lmx, xo[c][j]);
+        }
+      const int mwo = wave_max_i(lmx);
+      const float mw = key_of(mwo);
       float lsum = 0.0f;
       if (mw > -INFINITY) {
 #pragma unroll
         for (int c = 0; c < NC; ++c)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) lsum += (xv[c][j] > -INFINITY) ? expf(xv[c][j] - mw) : 0.0f;
+          for (int j = 0; j < 4; ++j) lsum += (xv[c][j] > -INFINITY) ? exp_fast(xv[c][j] - mw) : 0.0f;
       }
       const float sw = wave_sum(lsum);
       // lowest id holding the wave max (only the acoustic blank decision needs it)
@@ -408,7 +432,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         for (int c = NC - 1; c >= 0; --c) {
           unsigned long long mj[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) mj[j] = __ballot(xv[c][j] == mw && (c * W + g) * 4 + j < V);
+          for (int j = 0; j < 4; ++j) mj[j] = __ballot(xo[c][j] == mwo && (c * W + g) * 4 + j < V);
           const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
           if (any) {
             const int src = __ffsll((long long)any) - 1;
@@ -442,8 +466,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       if (y < V) {
         float v = as_float(a.y);
 #pragma unroll
-        for (int L2 = 3; L2 < kMaxLevels; ++L2)
-          if (L2 > L && L2 <= m) v = v + bo[L2];
+        for (int L2 = 3; L2 < kMaxLevels; ++L2) v = v + (L2 > L ? bo[L2] : 0.0f);
         lmval[y] = v;
         win16[2 * y] = (uint16_t)((L << 13) | j);
         if (L == N - 1 && j < kAux) sTN[j] = tnext;
@@ -481,7 +504,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const int bL = rdl(rw, rec_beg_lane(L)), cL = rdl(rw, rec_cnt_lane(L));
         const int done = min(cL, max(0, covered));
         covered -= cL;
-        const int2 *A = s_arcs[L] + bL;
+        const int2 *A = lm.arcs + bL;
         for (int j0 = done; j0 < cL; j0 += 4 * W) {
           int2 a4[4];
           int t4[4];
@@ -489,7 +512,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           for (int u = 0; u < 4; ++u) {
             const int j = j0 + u * W + g;
             a4[u] = j < cL ? A[j] : make_int2(INT_MAX, 0);
-            t4[u] = (L == N - 1 && j < cL && j < kAux) ? lm.top_next[bL + j] : 0;
+            t4[u] = (L == N - 1 && j < cL && j < kAux) ? lm.top_next[bL + j - lm.arc_base[N - 1]] : 0;
           }
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
@@ -507,7 +530,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       const bool wl = lane < NW;
       const float pm = wl ? s_pm[lane] : -INFINITY;
       const float M = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_max(pm)), 0));
-      const float term = (wl && pm > -INFINITY) ? s_ps[lane] * expf(pm - M) : 0.0f;
+      const float term = (wl && pm > -INFINITY) ? s_ps[lane] * exp_fast(pm - M) : 0.0f;
       lse = M + logf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_sum(term)), 0)));
       am = INT_MAX;
       if (p.mode == FUSION_BLANK_AM) {
@@ -545,11 +568,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           const float x = xv[c][j];
           const uint32_t lo = ww[j] & 0xFFFFu, hi = ww[j] >> 16;
           // LM: the scattered value if an arc won, else the dense row plus the
-          // backoffs of levels 2..m in increasing order
+          // backoffs of levels 2.. in increasing order
           float dres = lv[j];
 #pragma unroll
-          for (int L2 = 2; L2 < kMaxLevels; ++L2)
-            if (L2 <= m) dres = dres + bo[L2];
+          for (int L2 = 2; L2 < kMaxLevels; ++L2) dres = dres + bo[L2];
           const float lmv = lo ? lv[j] : dres;
           // phrases: the transition's entry value if this state overrides y, else the root's
           const int hidx = hi ? min((int)hi - 1, kAux - 1) : 0;
@@ -573,22 +595,28 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
     }
     // ---- the wave's top-k: per round the wave maximum of the remaining keys, then
-    // the lowest id holding it (ties to the lowest id); uniform values throughout --
+    // the lowest id holding it (ties to the lowest id); uniform values throughout.
+    // Keys compete as order-preserving ints; tokens that are not candidates or
+    // are already taken hold INT_MIN, below every key including -inf.
     {
+      int sk[NC][4];
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sk[c][j] = ((vm >> (c * 4 + j)) & 1u) ? ord_key(kk[c][j]) : INT_MIN;
       int r = 0;
       for (; r < K; ++r) {
-        float lb = -INFINITY;
+        int lb = INT_MIN;
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) lb = ((vm >> (c * 4 + j)) & 1u) ? fmaxf(lb, kk[c][j]) : lb;
-        const float M = wave_max(lb);
+        for (int c = 0; c < NC; ++c) lb = max(lb, max(max(sk[c][0], sk[c][1]), max(sk[c][2], sk[c][3])));
+        const int M = wave_max_i(lb);
+        if (M == INT_MIN) break;
         int wy = INT_MAX, wsrc = 0, wbit = 0;
 #pragma unroll
         for (int c = NC - 1; c >= 0; --c) {
           unsigned long long mj[4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) mj[j] = __ballot(((vm >> (c * 4 + j)) & 1u) && kk[c][j] == M);
+          for (int j = 0; j < 4; ++j) mj[j] = __ballot(sk[c][j] == M);
           const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
           if (any) {
             const int src = __ffsll((long long)any) - 1;
@@ -600,12 +628,15 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             wbit = c * 4 + jj;
           }
         }
-        if (wy == INT_MAX) break;
         if (lane == 0) {
           w_key[wave][r] = M;
           w_y[wave][r] = wy;
         }
-        if (lane == wsrc) vm &= ~(1u << wbit);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (wbit == c * 4 + j) sk[c][j] = (lane == wsrc) ? INT_MIN : sk[c][j];
       }
       if (lane == 0)
         for (; r < K; ++r) w_y[wave][r] = INT_MAX;
@@ -625,31 +656,40 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       s_steps += 1ull;
     }
     __syncthreads();
-    // ---- the hypothesis' top-k (wave 0): K DPP rounds over the NW sorted wave lists --
+    // ---- the hypothesis' top-k (wave 0): K rounds over the heads of the NW sorted
+    // wave lists (lanes 0..NW-1, one 16-lane row): DPP maximum of the keys, ties
+    // between waves to the lowest id ------------------------------------------------
     if (wave == 0) {
-      // lane w < NW holds wave w's list (best first)
-      float hk[KM];
-      int hy[KM];
+      int hk[KM], hy[KM];
 #pragma unroll
       for (int j = 0; j < KM; ++j) {
         const bool have = lane < NW && j < K;
         hy[j] = have ? w_y[lane][j] : INT_MAX;
-        hk[j] = (have && hy[j] != INT_MAX) ? w_key[lane][j] : -INFINITY;
+        hk[j] = (have && hy[j] != INT_MAX) ? w_key[lane][j] : INT_MIN;
       }
       // candidate j ends in lane j
-      float ck = -INFINITY;
-      int cy = INT_MAX;
+      int ck = INT_MIN, cy = INT_MAX;
       for (int j = 0; j < K; ++j) {
-        float k = hk[0];
-        int y = hy[0];
-        row_best(k, y);
-        const float bk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(k), 0));
-        const int by = __builtin_amdgcn_readlane(y, 0);
-        if (by == INT_MAX) break;
-        const unsigned long long own = __ballot(hy[0] == by && lane < NW);
-        const int src = __ffsll((long long)own) - 1;
+        int v = hk[0];
+        v = max(v, dpp_i<0xB1, 0xF>(v));
+        v = max(v, dpp_i<0x4E, 0xF>(v));
+        v = max(v, dpp_i<0x141, 0xF>(v));
+        v = max(v, dpp_i<0x140, 0xF>(v));
+        const int M = __builtin_amdgcn_readlane(v, 0);
+        if (M == INT_MIN) break;
+        const unsigned long long own = __ballot(lane < NW && hk[0] == M);
+        int src = __ffsll((long long)own) - 1;
+        int by = __builtin_amdgcn_readlane(hy[0], src);
+        for (unsigned long long rest = own & (own - 1); rest; rest &= rest - 1) {
+          const int l = __ffsll((long long)rest) - 1;
+          const int yl = __builtin_amdgcn_readlane(hy[0], l);
+          if (yl < by) {
+            by = yl;
+            src = l;
+          }
+        }
         if (lane == j) {
-          ck = bk;
+          ck = M;
           cy = by;
         }
         if (lane == src) {
@@ -658,12 +698,12 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             hk[i] = hk[i + 1];
             hy[i] = hy[i + 1];
           }
-          hk[KM - 1] = -INFINITY;
+          hk[KM - 1] = INT_MIN;
           hy[KM - 1] = INT_MAX;
         }
       }
       // each candidate lane resolves where its next state comes from (see HypState)
-      const float cf = ck - lse;
+      const float cf = cy != INT_MAX ? key_of(ck) - lse : -INFINITY;
       int cl = sid, cq = qid;
       if (cy != INT_MAX && cy != blank) {
         // the token's LDS tag word: LM winner level / offset, phrase transition
@@ -673,11 +713,18 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         if (lo) {
           const int L = (int)(lo >> 13), jj = (int)(lo & 0x1FFFu);
           const int bL = s_lbeg[L];
-          const long long sb = s_sbase[L];
-          cl = sb >= 0 ? (int)(sb + bL + jj) : (jj < kAux ? sTN[jj] : lm.top_next[bL + jj]);
+          cl = L < N - 1 ? (int)(s_sbase[L] + bL + jj)
+                         : (jj < kAux ? sTN[jj] : lm.top_next[bL + jj - lm.arc_base[N - 1]]);
         }
         cq = -1;
-        if (hi) cq = (int)hi - 1 < kAux ? sDT[hi - 1] : tr.delta[dbeg + (int)hi - 1].y;
+        if (hi) {
+          // LDS copy for the first kAux transitions, the table beyond; the table is
+          // read through a global-space pointer so the two loads stay distinct
+          // (a merged load would take the slower generic-address path)
+          const int4 __attribute__((address_space(1))) *gdelta =
+              (const int4 __attribute__((address_space(1))) *)tr.delta;
+          cq = (int)hi - 1 < kAux ? sDT[hi - 1] : gdelta[dbeg + (int)hi - 1].y;
+        }
         if (!p.has_trie) cq = 0;
       }
       if (p.step_mode) {
@@ -710,11 +757,14 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
       } else {
         // ---- beam: publish this hypothesis' candidates, meet the stream, rank all ----
+        // candidate record: (token, LM source, phrase source, parent's c_1) and
+        // (parent's flags, 0, total score S_b + fused as fp64)
         int4 *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * 2;
         if (lane < K) {
-          const double S0 = hs.S;
-          xs[(b * K + lane) * 2] = make_int4(as_int(cf), act ? cy : INT_MAX, cl, cq);
-          xs[(b * K + lane) * 2 + 1] = make_int4(hs.c1, hs.fl, __double2loint(S0), __double2hiint(S0));
+          const bool has = act && cy != INT_MAX;
+          const double tot = has ? hs.S + (double)cf : -INFINITY;
+          xs[(b * K + lane) * 2] = make_int4(has ? cy : INT_MAX, cl, cq, hs.c1);
+          xs[(b * K + lane) * 2 + 1] = make_int4(hs.fl, 0, __double2loint(tot), __double2hiint(tot));
         }
         int *cnt = p.counters + (size_t)sl * kCounterStride;
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -732,75 +782,50 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        // every workgroup of the stream ranks the same B*k candidates by
-        // (running score + fused desc, parent asc, rank asc); slot b takes rank b
+        // every workgroup of the stream ranks the same B*k candidates by (total
+        // desc, parent asc, rank asc), i.e. candidate order breaks ties; slot b
+        // takes rank b.  The totals are staged in LDS (NaN: no candidate, never
+        // ahead of anything) and each lane counts the candidates ahead of its own.
         const int nc = B * K;
-        int hit = 0, ry = 0, rl = 0, rq = 0, rc1 = 0, rfl = 0, rlo = 0, rhi = 0, rpar = 0;
-        for (int i0 = 0; i0 < nc; i0 += 64) {
-          const int i = i0 + lane;
-          int4 a = make_int4(0, INT_MAX, 0, 0), bb = make_int4(0, 0, 0, 0);
-          if (i < nc) {
-            a = xs[i * 2];
-            bb = xs[i * 2 + 1];
-          }
-          const bool valid = i < nc && a.y != INT_MAX;
-          const double sc = valid ? __hiloint2double(bb.w, bb.z) + (double)as_float(a.x) : -INFINITY;
-          int r = 0;
-          for (int j0 = 0; j0 < nc; j0 += 64) {
-            // candidates of block j0 broadcast by readlane (block i0 is in registers)
-            double scj = sc;
-            int vj = valid;
-            if (j0 != i0) {
-              const int jl = j0 + lane;
-              int4 a2 = make_int4(0, INT_MAX, 0, 0), b2 = make_int4(0, 0, 0, 0);
-              if (jl < nc) {
-                a2 = xs[jl * 2];
-                b2 = xs[jl * 2 + 1];
-              }
-              vj = jl < nc && a2.y != INT_MAX;
-              scj = vj ? __hiloint2double(b2.w, b2.z) + (double)as_float(a2.x) : -INFINITY;
+        for (int i = lane; i < nc; i += 64) {
+          const int4 a = xs[i * 2];
+          const int4 bb = xs[i * 2 + 1];
+          s_xa[i] = a;
+          s_xf[i] = bb.x;
+          s_tot[i] = a.x != INT_MAX ? __hiloint2double(bb.w, bb.z) : __longlong_as_double(0x7FF8000000000000ll);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        int wi = -1;
+        for (int i = lane; i < nc; i += 64) {
+          const double ti = s_tot[i];
+          if (ti == ti) {
+            int r = 0;
+#pragma unroll 16
+            for (int j = 0; j < nc; ++j) {
+              const double tj = s_tot[j];
+              r += (tj > ti || (tj == ti && j < i)) ? 1 : 0;
             }
-            const int n = min(64, nc - j0);
-            for (int u = 0; u < n; ++u) {
-              const int lo32 = __builtin_amdgcn_readlane(__double2loint(scj), u);
-              const int hi32 = __builtin_amdgcn_readlane(__double2hiint(scj), u);
-              const int vu = __builtin_amdgcn_readlane(vj, u);
-              const double s2 = __hiloint2double(hi32, lo32);
-              if (vu && (s2 > sc || (s2 == sc && j0 + u < i))) ++r;
-            }
-          }
-          if (valid && r == b) {
-            hit = 1;
-            ry = a.y;
-            rl = a.z;
-            rq = a.w;
-            rc1 = bb.x;
-            rfl = bb.y;
-            rlo = __double2loint(sc);
-            rhi = __double2hiint(sc);
-            rpar = i / K;
+            if (r == b) wi = i;
           }
         }
-        const unsigned long long bal = __ballot(hit);
         const int64_t o = (int64_t)t * H + h;
-        if (bal) {
-          const int src = __ffsll((long long)bal) - 1;
-          const int y = __builtin_amdgcn_readlane(ry, src), l = __builtin_amdgcn_readlane(rl, src);
-          const int q = __builtin_amdgcn_readlane(rq, src), c1p = __builtin_amdgcn_readlane(rc1, src);
-          const int pfl = __builtin_amdgcn_readlane(rfl, src), par = __builtin_amdgcn_readlane(rpar, src);
-          const int slo = __builtin_amdgcn_readlane(rlo, src), shi = __builtin_amdgcn_readlane(rhi, src);
-          if (lane == 0) {
-            hs.lmsrc = l;
-            hs.qsrc = q;
-            hs.y = y;
-            hs.c1p = c1p;
-            hs.c1 = y != blank ? y : c1p;
-            hs.fl = 1 | (pfl & 2);
-            hs.S = __hiloint2double(shi, slo);
-            p.tokens[o] = y;
-            p.parents[o] = par;
-          }
-        } else if (lane == 0) {
+        if (wi >= 0) {
+          // the lane holding the slot's candidate installs it
+          const int4 a = s_xa[wi];
+          const int y = a.x, c1p = a.w;
+          hs.lmsrc = a.y;
+          hs.qsrc = a.z;
+          hs.y = y;
+          hs.c1p = c1p;
+          hs.c1 = y != blank ? y : c1p;
+          hs.fl = 1 | (s_xf[wi] & 2);
+          hs.S = s_tot[wi];
+          p.tokens[o] = y;
+          p.parents[o] = wi / K;
+        }
+        if (__ballot(wi >= 0) == 0ull && lane == 0) {
           // no candidate reaches this slot: the hypothesis is dead and keeps its state
           hs.lmsrc = hs.cur_lm;
           hs.qsrc = hs.cur_q;

@@ -238,12 +238,20 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
       }
     }
   });
-  // ---- arcs of levels 2..N-1 (order L+1 n-grams) ---------------------------
-  std::vector<std::vector<int2>> arcs(N);
+  // ---- arcs of levels 2..N-1 (order L+1 n-grams), one array level by level -----
+  int64_t n_arcs = 0;
+  for (int L = 2; L <= N - 1; ++L) {
+    d.arc_base[L] = n_arcs;
+    n_arcs += ord[L + 1].n;
+  }
+  if (n_arcs > INT32_MAX) {
+    delete t;
+    return set_error(FUSION_E_UNSUPPORTED, "ngram_load: more than 2^31 n-grams of orders 3..N");
+  }
+  std::vector<int2> arcs((size_t)n_arcs);
   for (int L = 2; L <= N - 1; ++L) {
     const int k = L + 1;
-    arcs[L].resize(ord[k].n);
-    std::vector<int2> &A = arcs[L];
+    int2 *A = arcs.data() + d.arc_base[L];
     parallel_for(ord[k].n, [&](int64_t a, int64_t e) {
       for (int64_t i = a; i < e; ++i) {
         float p = lp_of(k, i);
@@ -271,7 +279,7 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
         }
         float bo = bo_of(m, i);
         std::memcpy(&r[2 + 3 * (m - 2)], &bo, 4);
-        r[2 + 3 * (m - 2) + 1] = (int32_t)arc_beg[m][i];
+        r[2 + 3 * (m - 2) + 1] = (int32_t)(d.arc_base[m] + arc_beg[m][i]);
         r[2 + 3 * (m - 2) + 2] = (int32_t)arc_cnt[m][i];
       }
     });
@@ -297,7 +305,7 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
   if (rc == FUSION_OK) rc = up.put(rec_dense, &d.rec_dense);
   if (rc == FUSION_OK) rc = up.put(cnt1, &d.cnt1);
   if (rc == FUSION_OK) rc = up.put(rec, &d.rec);
-  for (int L = 2; L <= N - 1 && rc == FUSION_OK; ++L) rc = up.put(arcs[L], &d.arcs[L]);
+  if (rc == FUSION_OK) rc = up.put(arcs, &d.arcs);
   if (rc == FUSION_OK) rc = up.put(top_next, &d.top_next);
   if (rc == FUSION_OK) {
     hipError_t e = hipStreamSynchronize(stream);
