@@ -204,8 +204,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   float *lmval = reinterpret_cast<float *>(dyn);
   uint32_t *win = reinterpret_cast<uint32_t *>(dyn) + Vp;
   uint16_t *win16 = reinterpret_cast<uint16_t *>(win);
-  float *sE = reinterpret_cast<float *>(dyn) + 2 * Vp;
-  int *sDT = reinterpret_cast<int *>(sE + kAux);
+  float *sE = reinterpret_cast<float *>(dyn) + 2 * Vp;  // sE[j + 1]: entry value of transition j
+  int *sDT = reinterpret_cast<int *>(sE + kAux + 4);
   int *sTN = sDT + kAux;
   __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves];
   __shared__ int s_paid[kMaxWaves];
@@ -285,6 +285,25 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   }
   __syncthreads();
 
+  // logits strip of this lane, raw (masked per frame): frame t+1's strip is
+  // fetched at the start of frame t, so it is in registers when t+1 begins
+  const int voff = g * 16;
+  float xraw[NC][4];
+  auto fetch_logits = [&](int tt) {
+    const rsrc_t xr = row_rsrc(p.logits + ((int64_t)tt * H + h) * p.V, p.V);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      if (AL) {
+        const float4 xx = row_load4(xr, voff, c * W * 16);
+        xraw[c][0] = xx.x; xraw[c][1] = xx.y; xraw[c][2] = xx.z; xraw[c][3] = xx.w;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) xraw[c][j] = row_load1(xr, voff + 4 * j, c * W * 16);
+      }
+    }
+  };
+  fetch_logits(0);
+
   bool aborted = false;  // after one failed rendezvous this workgroup stops waiting
   for (int t = 0; t < p.T; ++t) {
     const int V = uni(s_cfg[0]), blank = uni(s_cfg[1]);
@@ -300,7 +319,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     }
     const int lmsrc = uni(hs.lmsrc), qsrc = uni(hs.qsrc), yin = uni(hs.y);
     int c1 = uni(hs.c1);
-    // ---- hop 1: state record, phrase node, logits row ------------------------------
+    // ---- hop 1: state record, phrase node, dense level-1 row ---------------------
     const int32_t *rp = nullptr;
     if (ok) {
       if (lmsrc < 0) rp = lm.rec_dense + ((int64_t)uni(hs.c1p) * V + yin) * RS;
@@ -312,25 +331,12 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     if (rp && lane < RS) rw = rp[lane];
     if (np && lane >= kNodeLane && lane < kNodeLane + 4) rw = reinterpret_cast<const int *>(np)[lane - kNodeLane];
     const int64_t rowoff = ((int64_t)t * H + h) * V;
-    const int voff = g * 16;
     float xv[NC][4];
-    {
-      const rsrc_t xr = row_rsrc(p.logits + rowoff, act ? V : 0);
 #pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        const int y0 = (c * W + g) * 4;
-        if (AL) {
-          const float4 xx = row_load4(xr, voff, c * W * 16);
-          xv[c][0] = xx.x; xv[c][1] = xx.y; xv[c][2] = xx.z; xv[c][3] = xx.w;
-        } else {
+    for (int c = 0; c < NC; ++c)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) xv[c][j] = row_load1(xr, voff + 4 * j, c * W * 16);
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (!act || y0 + j >= V) xv[c][j] = -INFINITY;
-      }
-    }
+      for (int j = 0; j < 4; ++j) xv[c][j] = (act && (c * W + g) * 4 + j < V) ? xraw[c][j] : -INFINITY;
+    if (t + 1 < p.T) fetch_logits(t + 1);
     // the initial state of a run may need its record to learn c_1
     if (ok && c1 < 0) c1 = rp ? (rdl(rw, 0) & 0xFFFF) : lmsrc;
     // level-1 dense row straight into the LDS LM row; arcs scattered later overwrite it
@@ -349,6 +355,52 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             __builtin_amdgcn_global_load_lds(drow + (y < V ? y : 0), (lds_ptr_t)(lmval + wbase * 4 + j * 64), 4, 0, 0);
           }
         }
+      }
+    }
+    // ---- row statistics: wave max, sum of exp below it, raw argmax (while the
+    // state record is in flight) -------------------------------------------------
+    {
+      int xo[NC][4];  // order-preserving images of the logits (excluded tokens: -inf)
+      int lmx = INT_MIN;
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          xo[c][j] = ord_key(xv[c][j]);
+          lmx = max(lmx, xo[c][j]);
+        }
+      const int mwo = wave_max_i(lmx);
+      const float mw = key_of(mwo);
+      float lsum = 0.0f;
+      if (mw > -INFINITY) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) lsum += (xv[c][j] > -INFINITY) ? exp_fast(xv[c][j] - mw) : 0.0f;
+      }
+      const float sw = wave_sum(lsum);
+      // lowest id holding the wave max (only the acoustic blank decision needs it)
+      int aid = INT_MAX;
+      if (p.mode == FUSION_BLANK_AM && mw > -INFINITY) {
+#pragma unroll
+        for (int c = NC - 1; c >= 0; --c) {
+          unsigned long long mj[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) mj[j] = __ballot(xo[c][j] == mwo && (c * W + g) * 4 + j < V);
+          const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
+          if (any) {
+            const int src = __ffsll((long long)any) - 1;
+            int jj = 3;
+#pragma unroll
+            for (int j = 2; j >= 0; --j) jj = ((mj[j] >> src) & 1ull) ? j : jj;
+            aid = (c * W + wave * 64 + src) * 4 + jj;
+          }
+        }
+      }
+      if (lane == 0) {
+        s_pm[wave] = mw;
+        s_ps[wave] = sw;
+        s_paid[wave] = aid;
       }
     }
     // ---- decode the record ------------------------------------------------------
@@ -404,51 +456,6 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       dd[u] = make_int4(INT_MAX, 0, 0, 0);
       if (j < dcnt) dd[u] = tr.delta[dbeg + j];
     }
-    // ---- row statistics: wave max, sum of exp below it, raw argmax ----------------
-    {
-      int xo[NC][4];  // order-preserving images of the logits (excluded tokens: -inf)
-      int lmx = INT_MIN;
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          xo[c][j] = ord_key(xv[c][j]);
-          lmx = max(lmx, xo[c][j]);
-        }
-      const int mwo = wave_max_i(lmx);
-      const float mw = key_of(mwo);
-      float lsum = 0.0f;
-      if (mw > -INFINITY) {
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) lsum += (xv[c][j] > -INFINITY) ? exp_fast(xv[c][j] - mw) : 0.0f;
-      }
-      const float sw = wave_sum(lsum);
-      // lowest id holding the wave max (only the acoustic blank decision needs it)
-      int aid = INT_MAX;
-      if (p.mode == FUSION_BLANK_AM && mw > -INFINITY) {
-#pragma unroll
-        for (int c = NC - 1; c >= 0; --c) {
-          unsigned long long mj[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) mj[j] = __ballot(xo[c][j] == mwo && (c * W + g) * 4 + j < V);
-          const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
-          if (any) {
-            const int src = __ffsll((long long)any) - 1;
-            int jj = 3;
-#pragma unroll
-            for (int j = 2; j >= 0; --j) jj = ((mj[j] >> src) & 1ull) ? j : jj;
-            aid = (c * W + wave * 64 + src) * 4 + jj;
-          }
-        }
-      }
-      if (lane == 0) {
-        s_pm[wave] = mw;
-        s_ps[wave] = sw;
-        s_paid[wave] = aid;
-      }
-    }
     if (ok && g == 0) {
       hs.cur_lm = sid;
       hs.cur_q = qid;
@@ -479,7 +486,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         if (j < dcnt) {
           win16[2 * dd[u].x + 1] = (uint16_t)(j + 1);
           if (j < kAux) {
-            sE[j] = as_float(dd[u].z);
+            sE[j + 1] = as_float(dd[u].z);
             sDT[j] = dd[u].y;
           }
         }
@@ -488,7 +495,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const int4 e = tr.delta[dbeg + j];
         win16[2 * e.x + 1] = (uint16_t)(j + 1);
         if (j < kAux) {
-          sE[j] = as_float(e.z);
+          sE[j + 1] = as_float(e.z);
           sDT[j] = e.y;
         }
       }
@@ -543,6 +550,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     // ---- keys and the fused row ------------------------------------------------------
     const bool blank_only = inv || (p.mode == FUSION_BLANK_AM && am == blank);
     const bool want_keys = ok && (!blank_only || p.fused);
+    const bool compete = p.mode == FUSION_BLANK_COMPETE;
     const bool write_fused = p.fused != nullptr && ok;
     const rsrc_t fr = row_rsrc(write_fused ? p.fused + rowoff : p.logits, write_fused ? V : 0);
     float kk[NC][4];
@@ -552,9 +560,12 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       const int y0 = (c * W + g) * 4;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
+        // candidates: live tokens; blank only in blank-only frames or when it competes
+        // (bitwise logic: no per-token branches)
         const int y = y0 + j;
-        const bool cand = act && y < V && (blank_only ? y == blank : (p.mode == FUSION_BLANK_COMPETE || y != blank));
-        vm |= cand ? (1u << (c * 4 + j)) : 0u;
+        const bool is_blank = y == blank;
+        const bool cand = act & (y < V) & (blank_only ? is_blank : (compete | !is_blank));
+        vm |= (uint32_t)cand << (c * 4 + j);
         kk[c][j] = xv[c][j];
       }
       if (want_keys) {
@@ -562,6 +573,20 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const float4 l4 = *reinterpret_cast<const float4 *>(lmval + y0);
         const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
         const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        // the phrase entry values: the LDS copy of the state's first kAux transitions
+        // (read for every token, index 0 when unused, so that no per-token branch
+        // guards the read), the delta table beyond them only for a state with more
+        float eh[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) eh[j] = sE[min((int)(ww[j] >> 16), kAux)];
+        asm volatile("" ::"v"(eh[0]), "v"(eh[1]), "v"(eh[2]), "v"(eh[3]));
+        if (dcnt > kAux) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int hi = (int)(ww[j] >> 16);
+            if (hi > kAux) eh[j] = as_float(tr.delta[dbeg + hi - 1].z);
+          }
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int y = y0 + j;
@@ -574,9 +599,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           for (int L2 = 2; L2 < kMaxLevels; ++L2) dres = dres + bo[L2];
           const float lmv = lo ? lv[j] : dres;
           // phrases: the transition's entry value if this state overrides y, else the root's
-          const int hidx = hi ? min((int)hi - 1, kAux - 1) : 0;
-          float e = hi ? sE[hidx] : rE[c][j];
-          if ((int)hi > kAux) e = as_float(tr.delta[dbeg + (int)hi - 1].z);
+          const float e = hi ? eh[j] : rE[c][j];
           const float bst = e - phiq;
           const float a1 = p.lam * lmv;
           const float a2 = x + a1;
@@ -927,7 +950,7 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   KernelFn fn = pick(sh, km, al);
   const DeviceInfo di = device_info();
   if (!di.ok) return set_error(FUSION_E_HIP, "cannot query the device");
-  const size_t dyn = (size_t)4 * (2 * sh.Vp + 3 * kAux);
+  const size_t dyn = (size_t)4 * (2 * sh.Vp + 3 * kAux + 4);
   hipFuncAttributes attr;
   hipError_t e = hipFuncGetAttributes(&attr, reinterpret_cast<const void *>(fn));
   if (e != hipSuccess) return hip_error(e, "hipFuncGetAttributes");
