@@ -679,51 +679,47 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       s_steps += 1ull;
     }
     __syncthreads();
-    // ---- the hypothesis' top-k (wave 0): K rounds over the heads of the NW sorted
-    // wave lists (lanes 0..NW-1, one 16-lane row): DPP maximum of the keys, ties
-    // between waves to the lowest id ------------------------------------------------
+    // ---- the hypothesis' top-k (wave 0): the K-entry lists of the NW waves spread
+    // over the lanes (entry j of wave w is element e = j*NW + w, lane e % 64, slot
+    // e / 64); K rounds of a wave maximum, ties to the lowest id -------------------
     if (wave == 0) {
-      int hk[KM], hy[KM];
+      constexpr int kSlots = (kMaxWaves * KM + 63) / 64;
+      int ek[kSlots], ey[kSlots];
 #pragma unroll
-      for (int j = 0; j < KM; ++j) {
-        const bool have = lane < NW && j < K;
-        hy[j] = have ? w_y[lane][j] : INT_MAX;
-        hk[j] = (have && hy[j] != INT_MAX) ? w_key[lane][j] : INT_MIN;
+      for (int q = 0; q < kSlots; ++q) {
+        const int e = q * 64 + lane;
+        const int w = e % NW, j = e / NW;
+        ey[q] = j < K ? w_y[w][j] : INT_MAX;
+        ek[q] = (j < K && ey[q] != INT_MAX) ? w_key[w][j] : INT_MIN;
       }
       // candidate j ends in lane j
       int ck = INT_MIN, cy = INT_MAX;
       for (int j = 0; j < K; ++j) {
-        int v = hk[0];
-        v = max(v, dpp_i<0xB1, 0xF>(v));
-        v = max(v, dpp_i<0x4E, 0xF>(v));
-        v = max(v, dpp_i<0x141, 0xF>(v));
-        v = max(v, dpp_i<0x140, 0xF>(v));
-        const int M = __builtin_amdgcn_readlane(v, 0);
+        int v = ek[0];
+#pragma unroll
+        for (int q = 1; q < kSlots; ++q) v = max(v, ek[q]);
+        const int M = wave_max_i(v);
         if (M == INT_MIN) break;
-        const unsigned long long own = __ballot(lane < NW && hk[0] == M);
-        int src = __ffsll((long long)own) - 1;
-        int by = __builtin_amdgcn_readlane(hy[0], src);
-        for (unsigned long long rest = own & (own - 1); rest; rest &= rest - 1) {
-          const int l = __ffsll((long long)rest) - 1;
-          const int yl = __builtin_amdgcn_readlane(hy[0], l);
-          if (yl < by) {
-            by = yl;
-            src = l;
+        int by = INT_MAX, bl = 0, bq = 0;
+#pragma unroll
+        for (int q = 0; q < kSlots; ++q) {
+          for (unsigned long long own = __ballot(ek[q] == M); own; own &= own - 1) {
+            const int l = __ffsll((long long)own) - 1;
+            const int yl = __builtin_amdgcn_readlane(ey[q], l);
+            if (yl < by) {
+              by = yl;
+              bl = l;
+              bq = q;
+            }
           }
         }
         if (lane == j) {
           ck = M;
           cy = by;
         }
-        if (lane == src) {
 #pragma unroll
-          for (int i = 0; i < KM - 1; ++i) {
-            hk[i] = hk[i + 1];
-            hy[i] = hy[i + 1];
-          }
-          hk[KM - 1] = INT_MIN;
-          hy[KM - 1] = INT_MAX;
-        }
+        for (int q = 0; q < kSlots; ++q)
+          if (q == bq && lane == bl) ek[q] = INT_MIN;
       }
       // each candidate lane resolves where its next state comes from (see HypState)
       const float cf = cy != INT_MAX ? key_of(ck) - lse : -INFINITY;
