@@ -27,6 +27,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
 METRIC = "fused hyp×vocab scores/sec + decode steps/sec; achieved HBM GB/s vs peak"
 
 
@@ -82,6 +83,7 @@ def main():
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--fused", action="store_true", help="also write the full fused score rows")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--no-projection", action="store_true", help="skip the joint-projection measurement")
     ap.add_argument("--cpu-frames", type=int, default=300)
     ap.add_argument("--cpu-streams", type=int, default=64)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -208,6 +210,40 @@ def main():
         },
         "cpu_baseline": None,
     }
+    # the joint output projection (bf16 MFMA) that would produce this run's logits:
+    # [T*H, 640] x [640, V], timed on its own; not part of the step above
+    if not args.no_projection:
+        from workloads import make_projection
+
+        A, Wt, bias = make_projection(args.config)
+        M, K = A.shape
+        N = Wt.shape[0]
+        a_d = torch.from_numpy(A.view(np.int16)).to(dev)
+        w_d = torch.from_numpy(Wt.view(np.int16)).to(dev)
+        b_d = torch.from_numpy(bias).to(dev)
+        o_d = torch.empty((M, N), dtype=torch.float32, device=dev)
+        for _ in range(3):
+            F.joint_project(a_d, w_d, b_d, M, N, K, o_d, stream.cuda_stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n_rep = 10
+        e0.record(stream)
+        for _ in range(n_rep):
+            F.joint_project(a_d, w_d, b_d, M, N, K, o_d, stream.cuda_stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pms = e0.elapsed_time(e1) / n_rep
+        flops = 2.0 * M * N * K
+        pbytes = 2.0 * M * K + 2.0 * N * K + 4.0 * N + 4.0 * M * N
+        out["projection"] = {
+            "kernel": "joint_proj_kernel", "shape": [M, N, K], "ms_per_launch": pms,
+            "tflops": flops / (pms / 1e3) / 1e12, "peak_tflops_bf16": BF16_PEAK_TFLOPS,
+            "frac_of_peak": flops / (pms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
+            "min_hbm_bytes": pbytes, "hbm_gbs_at_min_bytes": pbytes / (pms / 1e3) / 1e9,
+        }
+        log(f"joint projection {M}x{N}x{K}: {pms:.3f} ms, {flops / (pms / 1e3) / 1e12:.1f} TFLOP/s")
+        del a_d, w_d, b_d, o_d
+
     rec = recorded_traffic(w.name)
     digest = kernel_sources_digest()
     if rec is None:

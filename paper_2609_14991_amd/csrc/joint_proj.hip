@@ -7,12 +7,12 @@
 // A is [M, K] and W is [N, K], both row-major bf16 (W in the usual layout of a
 // linear layer's weight), so both MFMA operands are contiguous along K.
 //
-// Tiling for gfx950: a 256-lane workgroup computes a 128 x 128 output tile as
-// 4 waves of 64 x 64, each a 4 x 4 grid of v_mfma_f32_16x16x32_bf16 tiles
-// (64 fp32 accumulators per lane).  K advances in stages of 32: every lane
-// fetches two 16-byte strips of A and two of W per stage into registers while
-// the previous stage, double-buffered in LDS (rows padded by 16 bytes), feeds
-// the MFMAs.  Tiles are numbered column-fastest, so with the hardware's
+// Tiling for gfx950: a workgroup of WM x WN waves computes a (64 WM) x (64 WN)
+// output tile, each wave 64 x 64 as a 4 x 4 grid of v_mfma_f32_16x16x32_bf16
+// tiles (64 fp32 accumulators per lane).  K advances in stages of BK: every
+// lane fetches its 16-byte strips of A and W for the next stage into registers
+// while the current stage, double-buffered in LDS (rows padded by 16 bytes),
+// feeds the MFMAs.  Tiles are numbered column-fastest, so with the hardware's
 // round-robin of workgroups over the 8 XCDs each XCD's L2 holds a quarter of W.
 #include <hip/hip_runtime.h>
 
@@ -27,51 +27,63 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBM = 128, kBN = 128, kBK = 32;
-constexpr int kLd = kBK + 8;  // bf16 per LDS row: 80 bytes
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-__global__ void __launch_bounds__(256) joint_proj_kernel(const uint16_t *__restrict__ A,
-                                                          const uint16_t *__restrict__ W,
-                                                          const float *__restrict__ bias, int M, int N, int K,
-                                                          int n_col_tiles, float *__restrict__ out) {
-  __shared__ __align__(16) uint16_t sA[2][kBM * kLd];
-  __shared__ __align__(16) uint16_t sW[2][kBN * kLd];
+// kWM x kWN waves, each a 64 x 64 output tile; K stages of kBK
+template <int kWM, int kWN, int kBK>
+__global__ void __launch_bounds__(64 * kWM * kWN) joint_proj_kernel(const uint16_t *__restrict__ A,
+                                                                     const uint16_t *__restrict__ W,
+                                                                     const float *__restrict__ bias, int M, int N,
+                                                                     int K, int n_col_tiles, int vec_out,
+                                                                     float *__restrict__ out) {
+  constexpr int kBM = 64 * kWM, kBN = 64 * kWN;
+  constexpr int kLd = kBK + 8;  // bf16 per LDS row (16-byte pad)
+  constexpr int kThreads = 64 * kWM * kWN;
+  constexpr int kStripsA = kBM * kBK / 8 / kThreads;  // 16-byte strips per thread and stage
+  constexpr int kStripsW = kBN * kBK / 8 / kThreads;
+  constexpr int kChunks = kBK / 8;                     // strips per row
+  // one LDS block: the double-buffered operand stages, reused by the epilogue
+  __shared__ __align__(16) uint16_t smem[2 * (kBM + kBN) * kLd];
+  uint16_t(*sA)[kBM * kLd] = reinterpret_cast<uint16_t(*)[kBM * kLd]>(smem);
+  uint16_t(*sW)[kBN * kLd] = reinterpret_cast<uint16_t(*)[kBN * kLd]>(smem + 2 * kBM * kLd);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int tile = blockIdx.x;
   const int bn = (tile % n_col_tiles) * kBN, bm = (tile / n_col_tiles) * kBM;
-  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+  const int wm = (wave / kWN) * 64, wn = (wave % kWN) * 64;
 
   // reads past a row range or past K return zeros (buffer range check)
   const __amdgpu_buffer_rsrc_t ra = rsrc(A, (uint32_t)((int64_t)M * K * 2));
   const __amdgpu_buffer_rsrc_t rw = rsrc(W, (uint32_t)((int64_t)N * K * 2));
-  // strip c = tid + 256 * i (i < 2) of a 128 x 32 stage: row c >> 2, K offset (c & 3) * 8
-  int arow[2], kc[2];
+  // strip c = tid + kThreads * i of a stage: row c / kChunks, K offset (c % kChunks) * 8
+  auto fetch = [&](int k0, i32x4 (&ga)[kStripsA], i32x4 (&gw)[kStripsW]) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int c = tid + 256 * i;
-    arow[i] = c >> 2;
-    kc[i] = (c & 3) * 8;
-  }
-  auto fetch = [&](int k0, i32x4 (&ga)[2], i32x4 (&gw)[2]) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int k = k0 + kc[i];
-      const int m = bm + arow[i], n = bn + arow[i];
+    for (int i = 0; i < kStripsA; ++i) {
+      const int c = tid + kThreads * i;
+      const int k = k0 + (c % kChunks) * 8, m = bm + c / kChunks;
       const uint32_t oa = (m < M && k < K) ? (uint32_t)(((int64_t)m * K + k) * 2) : 0xFFFFFFF0u;
-      const uint32_t ow = (n < N && k < K) ? (uint32_t)(((int64_t)n * K + k) * 2) : 0xFFFFFFF0u;
       ga[i] = __builtin_amdgcn_raw_buffer_load_b128(ra, oa, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < kStripsW; ++i) {
+      const int c = tid + kThreads * i;
+      const int k = k0 + (c % kChunks) * 8, n = bn + c / kChunks;
+      const uint32_t ow = (n < N && k < K) ? (uint32_t)(((int64_t)n * K + k) * 2) : 0xFFFFFFF0u;
       gw[i] = __builtin_amdgcn_raw_buffer_load_b128(rw, ow, 0, 0);
     }
   };
-  auto stash = [&](int buf, const i32x4 (&ga)[2], const i32x4 (&gw)[2]) {
+  auto stash = [&](int buf, const i32x4 (&ga)[kStripsA], const i32x4 (&gw)[kStripsW]) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      *reinterpret_cast<i32x4 *>(&sA[buf][arow[i] * kLd + kc[i]]) = ga[i];
-      *reinterpret_cast<i32x4 *>(&sW[buf][arow[i] * kLd + kc[i]]) = gw[i];
+    for (int i = 0; i < kStripsA; ++i) {
+      const int c = tid + kThreads * i;
+      *reinterpret_cast<i32x4 *>(&sA[buf][(c / kChunks) * kLd + (c % kChunks) * 8]) = ga[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kStripsW; ++i) {
+      const int c = tid + kThreads * i;
+      *reinterpret_cast<i32x4 *>(&sW[buf][(c / kChunks) * kLd + (c % kChunks) * 8]) = gw[i];
     }
   };
 
@@ -83,7 +95,7 @@ __global__ void __launch_bounds__(256) joint_proj_kernel(const uint16_t *__restr
 
   const int nk = (K + kBK - 1) / kBK;
   {
-    i32x4 ga[2], gw[2];
+    i32x4 ga[kStripsA], gw[kStripsW];
     fetch(0, ga, gw);
     stash(0, ga, gw);
   }
@@ -92,35 +104,70 @@ __global__ void __launch_bounds__(256) joint_proj_kernel(const uint16_t *__restr
   const int fr = lane & 15, fk = (lane >> 4) * 8;
   for (int kt = 0; kt < nk; ++kt) {
     const int buf = kt & 1;
-    i32x4 ga[2], gw[2];
+    i32x4 ga[kStripsA], gw[kStripsW];
     const bool more = kt + 1 < nk;
     if (more) fetch((kt + 1) * kBK, ga, gw);
-    bf16x8 fa[4], fw[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      fa[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][(wm + i * 16 + fr) * kLd + fk]);
-      fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[buf][(wn + i * 16 + fr) * kLd + fk]);
+    for (int ks = 0; ks < kBK; ks += 32) {
+      bf16x8 fa[4], fw[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        fa[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][(wm + i * 16 + fr) * kLd + ks + fk]);
+        fw[i] = *reinterpret_cast<const bf16x8 *>(&sW[buf][(wn + i * 16 + fr) * kLd + ks + fk]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fw[j], acc[i][j], 0, 0, 0);
     }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[i], fw[j], acc[i][j], 0, 0, 0);
     if (more) stash(buf ^ 1, ga, gw);
     __syncthreads();
   }
 
   // accumulator of a 16 x 16 tile: lane l holds column l % 16, rows 4 * (l / 16) .. + 3
+  if (vec_out) {
+    // each 16-row slab of the wave's tile goes through the wave's own LDS area
+    // (the operand buffers are free after the last stage) and leaves as whole
+    // rows: 16 lanes store one row of 64 floats with 16-byte stores
+    constexpr int kSlabLd = 64 + 4;
+    float *slab = reinterpret_cast<float *>(smem) + wave * 16 * kSlabLd;
+    static_assert(sizeof(smem) >= sizeof(float) * 16 * kSlabLd * kWM * kWN, "LDS too small for the epilogue");
+    float bv[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int n = bn + wn + j * 16 + (lane & 15);
-    if (n >= N) continue;
-    const float bv = bias ? bias[n] : 0.0f;
+    for (int j = 0; j < 4; ++j) {
+      const int n = bn + wn + j * 16 + (lane & 15);
+      bv[j] = (bias && n < N) ? bias[n] : 0.0f;
+    }
+    const int cn = bn + wn + (lane & 15) * 4;  // first of the 4 columns this lane stores
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int m = bm + wm + i * 16 + (lane >> 4) * 4 + r;
-        if (m < M) out[(int64_t)m * N + n] = acc[i][j][r] + bv;
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) slab[((lane >> 4) * 4 + r) * kSlabLd + j * 16 + (lane & 15)] = acc[i][j][r] + bv[j];
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int row = q * 4 + (lane >> 4);
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(&slab[row * kSlabLd + (lane & 15) * 4]);
+        const int m = bm + wm + i * 16 + row;
+        if (m < M && cn < N) *reinterpret_cast<f32x4 *>(&out[(int64_t)m * N + cn]) = v;
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = bn + wn + j * 16 + (lane & 15);
+      if (n >= N) continue;
+      const float bv = bias ? bias[n] : 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = bm + wm + i * 16 + (lane >> 4) * 4 + r;
+          if (m < M) out[(int64_t)m * N + n] = acc[i][j][r] + bv;
+        }
       }
     }
   }
@@ -140,9 +187,14 @@ extern "C" int joint_project(const uint16_t *A, const uint16_t *W, const float *
   if (M == 0) return FUSION_OK;
   if (!A || !W || !out) return set_error(FUSION_E_ARG, "NULL operand");
   if (((uintptr_t)A | (uintptr_t)W) % 16 != 0) return set_error(FUSION_E_ARG, "A and W must be 16-byte aligned");
-  const int nct = (N + kBN - 1) / kBN, nrt = (M + kBM - 1) / kBM;
+  constexpr int WM = 2, WN = 4, BK = 32;  // 128 x 256 tiles, 8 waves, K stages of 32
+  constexpr int BM = 64 * WM, BN = 64 * WN;
+  const int nct = (N + BN - 1) / BN, nrt = (M + BM - 1) / BM;
   if ((int64_t)nct * nrt > 0x7FFFFFFFll) return set_error(FUSION_E_UNSUPPORTED, "too many tiles");
-  hipLaunchKernelGGL(joint_proj_kernel, dim3(nct * nrt), dim3(256), 0, stream, A, W, bias, M, N, K, nct, out);
+  // whole 16-byte row segments when every row starts 16-byte aligned
+  const int vec_out = (N % 4 == 0 && (uintptr_t)out % 16 == 0) ? 1 : 0;
+  hipLaunchKernelGGL((joint_proj_kernel<WM, WN, BK>), dim3(nct * nrt), dim3(64 * WM * WN), 0, stream, A, W, bias, M,
+                     N, K, nct, vec_out, out);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? FUSION_OK : hip_error(e, "joint projection launch");
 }

@@ -17,6 +17,8 @@ the LM adds ``BOS = V`` and ``EOS = V + 1``.
 from __future__ import annotations
 
 import functools
+import os
+import sys
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -147,6 +149,12 @@ def make_corpus(rng, n_sent: int, V: int, s: float, blank: int = 0, len_range=(5
 # --------------------------------------------------------------------------
 # Kneser-Ney estimation (workload tool: produces the LM the method consumes)
 # --------------------------------------------------------------------------
+def _progress(msg):
+    """Progress of the slow estimation steps, when FUSION_WORKLOAD_PROGRESS=1."""
+    if os.environ.get("FUSION_WORKLOAD_PROGRESS") == "1":
+        print(f"[workloads] {msg}", file=sys.stderr, flush=True)
+
+
 def _count_ngrams(tokens, offsets, V, N):
     """Distinct n-grams (as base-(V+2) packed keys, sorted) and raw counts per order."""
     base = V + 2
@@ -178,6 +186,7 @@ def _count_ngrams(tokens, offsets, V, N):
         u, c = np.unique(sel, return_counts=True)
         uniq[k], raw[k] = u, c.astype(np.int64)
         del sel
+        _progress(f"order {k}: {u.size} distinct n-grams counted")
     return uniq, raw
 
 
@@ -248,6 +257,7 @@ def estimate_kn(tokens, offsets, V: int, N: int, cutoffs, blank: int = 0) -> LMA
     kept_p = {1: p_uni[uni_ids]}
     bo = {}
     for k in range(2, N + 1):
+        _progress(f"order {k}: estimating")
         u, c, r = uniq[k], kn[k], raw[k]
         d = _discount(c)
         ctx = u // base
@@ -378,20 +388,22 @@ def make_projection(cfg: int = 5, M: int | None = None, K: int = 640, N: int | N
 
 
 @functools.lru_cache(maxsize=2)
-def _corpus_and_lm(lm_seed: int):
+def _corpus_and_lm(lm_seed: int, n_sent: int):
     c = CONFIGS[lm_seed]
     rng = seed_streams(lm_seed)[0]
-    toks, offs = make_corpus(rng, c["n_sent"], c["V"], c["zipf"])
+    toks, offs = make_corpus(rng, n_sent, c["V"], c["zipf"])
     lm = estimate_kn(toks, offs, c["V"], c["N"], c["cutoffs"])
     return toks, offs, lm
 
 
 def load_workload(cfg: int, T: int | None = None, S: int | None = None,
-                  with_logits: bool = True) -> Workload:
+                  with_logits: bool = True, n_sent: int | None = None) -> Workload:
     """Build workload ``cfg`` (1..5).  ``T``/``S`` shrink the frame or stream
-    count (the LM and phrase list stay the full ones)."""
+    count (the LM and phrase list stay the full ones); ``n_sent`` replaces the
+    corpus size the LM is estimated from (same order, cutoffs and seeds)."""
     c = CONFIGS[cfg]
-    toks, offs, lm = _corpus_and_lm(c["lm_seed"])
+    ns = c["n_sent"] if n_sent is None else int(n_sent)
+    toks, offs, lm = _corpus_and_lm(c["lm_seed"], ns)
     _, r_phr, r_log, r_peak, _ = seed_streams(cfg)
     phr = make_phrases(r_phr, c["n_phr"], c["plen"], toks, offs, c["V"])
     T_full, S_full = c["T"], c["S"]
@@ -405,7 +417,7 @@ def load_workload(cfg: int, T: int | None = None, S: int | None = None,
     return Workload(cfg=cfg, name=c["name"], V=c["V"], N=c["N"], blank=0, lm=lm, phrases=phr,
                     S=S_, B=c["B"], T=T_, k=c["k"], lam=c["lam"], beta=c["beta"],
                     chunk=c["chunk"], logits=logits,
-                    meta=dict(ngram_counts=lm.counts, n_sent=c["n_sent"], zipf=c["zipf"],
+                    meta=dict(ngram_counts=lm.counts, n_sent=ns, zipf=c["zipf"],
                               cutoffs=list(c["cutoffs"]), n_phrases=c["n_phr"]))
 
 
