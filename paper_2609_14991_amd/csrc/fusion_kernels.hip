@@ -56,8 +56,7 @@ constexpr int kMaxWaves = 16;
 constexpr int kMaxLevels = FUSION_MAX_ORDER;  // context levels 1..N-1 <= 7
 constexpr int kAux = 256;                     // LDS side tables: phrase transitions, top-level next states
 constexpr int kNodeLane = 32;                 // lanes 32..35 of the record word hold the phrase node
-constexpr int kCounterStride = 16;            // ints between per-stream counters (one 64-byte line)
-constexpr int kSpinLimit = 1 << 20;           // bounded wait at the beam rendezvous (~1 s)
+constexpr int kSpinLimit = 1 << 20;           // bounded wait at the beam rendezvous (polls, ~1 s)
 
 __device__ int g_status;
 
@@ -75,8 +74,7 @@ struct Params {
   float *scores;  // fusion_step outputs [H, k]
   int32_t *next_lm;
   int32_t *next_boost;
-  int4 *xchg;     // beam exchange [S][2][B][k] candidate records of two int4
-  int *counters;  // [S * kCounterStride]
+  unsigned long long *xchg;  // beam exchange [S][2][B][k] candidate records of four tagged words
   int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, pad;
   float lam, beta;
 };
@@ -776,42 +774,63 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
       } else {
         // ---- beam: publish this hypothesis' candidates, meet the stream, rank all ----
-        // candidate record: (token, LM source, phrase source, parent's c_1) and
-        // (parent's flags, 0, total score S_b + fused as fp64)
-        int4 *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * 2;
+        // A candidate record is four 64-bit words, each carrying the frame tag in
+        // its top 16 bits over 48 bits of payload: the total score S_b + fused
+        // (fp64), the LM and phrase sources, the token and the parent's c_1 and
+        // flags.  Words are written and read as relaxed agent-scope atomics, so a
+        // reader that sees the current tag in all four words holds the whole
+        // record: polling the records is the rendezvous (no counter, no fence).
+        // Frames alternate between two buffers; a writer can be at most one frame
+        // ahead of any reader of its stream, so it never overwrites a buffer that
+        // is still being read.
+        unsigned long long *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * 4;
+        const unsigned long long tag = (unsigned long long)((t + 1) & 0xFFFF) << 48;
+        constexpr unsigned long long kPay = (1ull << 48) - 1;
         if (lane < K) {
           const bool has = act && cy != INT_MAX;
           const double tot = has ? hs.S + (double)cf : -INFINITY;
-          xs[(b * K + lane) * 2] = make_int4(has ? cy : INT_MAX, cl, cq, hs.c1);
-          xs[(b * K + lane) * 2 + 1] = make_int4(hs.fl, 0, __double2loint(tot), __double2hiint(tot));
+          const unsigned long long tb = (unsigned long long)__double_as_longlong(tot);
+          const unsigned long long w[4] = {
+              (tb & kPay) | tag,
+              (tb >> 48) | ((unsigned long long)(unsigned)cl << 16) | tag,
+              (unsigned long long)(unsigned)cq | ((unsigned long long)(has ? cy + 1 : 0) << 32) | tag,
+              (unsigned long long)((hs.c1 + 1) & 0xFFFF) | ((unsigned long long)(hs.fl & 0xFF) << 16) | tag};
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            __hip_atomic_store(xs + (b * K + lane) * 4 + q, w[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        int *cnt = p.counters + (size_t)sl * kCounterStride;
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-        if (lane == 0) {
-          __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          const int target = B * (t + 1);
-          int spins = 0;
-          while (!aborted && __hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            if (++spins > kSpinLimit) {
-              atomicOr(&g_status, FUSION_STATUS_SYNC_TIMEOUT);
-              aborted = true;
-            }
-            __builtin_amdgcn_s_sleep(1);
-          }
-        }
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         // every workgroup of the stream ranks the same B*k candidates by (total
         // desc, parent asc, rank asc), i.e. candidate order breaks ties; slot b
         // takes rank b.  The totals are staged in LDS (NaN: no candidate, never
         // ahead of anything) and each lane counts the candidates ahead of its own.
         const int nc = B * K;
-        for (int i = lane; i < nc; i += 64) {
-          const int4 a = xs[i * 2];
-          const int4 bb = xs[i * 2 + 1];
-          s_xa[i] = a;
-          s_xf[i] = bb.x;
-          s_tot[i] = a.x != INT_MAX ? __hiloint2double(bb.w, bb.z) : __longlong_as_double(0x7FF8000000000000ll);
+        for (int i0 = 0; i0 < nc; i0 += 64) {
+          const int i = i0 + lane;
+          unsigned long long w[4] = {0ull, 0ull, 0ull, 0ull};
+          bool cur = i >= nc;
+          for (int spins = 0;; ++spins) {
+            if (i < nc) {
+#pragma unroll
+              for (int q = 0; q < 4; ++q) w[q] = __hip_atomic_load(xs + i * 4 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              cur = (w[0] & ~kPay) == tag && (w[1] & ~kPay) == tag && (w[2] & ~kPay) == tag && (w[3] & ~kPay) == tag;
+            }
+            if (__ballot(!cur) == 0ull || aborted) break;
+            if (spins >= kSpinLimit) {
+              if (lane == 0) atomicOr(&g_status, FUSION_STATUS_SYNC_TIMEOUT);
+              aborted = true;
+              break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+          }
+          if (i < nc) {
+            const int y1 = (int)((w[2] >> 32) & 0xFFFF);
+            const bool valid = cur && y1 != 0;
+            s_xa[i] = make_int4(y1 - 1, (int)(unsigned)((w[1] >> 16) & 0xFFFFFFFFull), (int)(unsigned)(w[2] & 0xFFFFFFFFull),
+                                (int)(w[3] & 0xFFFF) - 1);
+            s_xf[i] = (int)((w[3] >> 16) & 0xFF);
+            s_tot[i] = valid ? __longlong_as_double((long long)((w[0] & kPay) | ((w[1] & 0xFFFF) << 48)))
+                             : __longlong_as_double(0x7FF8000000000000ll);
+          }
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
         __builtin_amdgcn_wave_barrier();
@@ -970,20 +989,23 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   int s_batch = (int)std::min<long>(p.S, resident / p.B);
   if (s_batch >= 8) s_batch -= s_batch % 8;
   if (s_batch < 1) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device at once");
-  const size_t xbytes = (size_t)s_batch * 2 * p.B * p.k * 2 * sizeof(int4);
-  const size_t cbytes = (size_t)s_batch * kCounterStride * sizeof(int);
+  // exchange records: 2 buffers x B x k candidates x 4 words per stream
+  const size_t xwords = (size_t)s_batch * 2 * p.B * p.k * 4;
   void *scratch = nullptr;
-  e = hipMallocAsync(&scratch, xbytes + cbytes, stream);
+  e = hipMallocAsync(&scratch, xwords * sizeof(unsigned long long), stream);
   if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
-  p.xchg = reinterpret_cast<int4 *>(scratch);
-  p.counters = reinterpret_cast<int *>(reinterpret_cast<char *>(scratch) + xbytes);
+  p.xchg = reinterpret_cast<unsigned long long *>(scratch);
   int rc = FUSION_OK;
   for (int s0 = 0; s0 < p.S && rc == FUSION_OK; s0 += s_batch) {
     const int ns = std::min(s_batch, p.S - s0);
-    hipLaunchKernelGGL(zero_ints, dim3(1), dim3(256), 0, stream, p.counters, s_batch * kCounterStride);
+    // tag 0 (no frame uses it) everywhere, so that neither uninitialised memory
+    // nor an earlier batch's records can pass for the current frame's
+    const int n_ints = (int)(xwords * 2);
+    hipLaunchKernelGGL(zero_ints, dim3(std::min(64, (n_ints + 255) / 256)), dim3(256), 0, stream,
+                       reinterpret_cast<int *>(scratch), n_ints);
     e = hipGetLastError();
     if (e != hipSuccess) {
-      rc = hip_error(e, "counter reset launch");
+      rc = hip_error(e, "exchange reset launch");
       break;
     }
     Params q = p;
