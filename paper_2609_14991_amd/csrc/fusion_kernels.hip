@@ -616,51 +616,61 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
     }
     // ---- the wave's top-k: per round the wave maximum of the remaining keys, then
-    // the lowest id holding it (ties to the lowest id); uniform values throughout.
-    // Keys compete as order-preserving ints; tokens that are not candidates or
-    // are already taken hold INT_MIN, below every key including -inf.
+    // the lowest id holding it (ties to the lowest id).  Keys compete as
+    // order-preserving ints; tokens that are not candidates or are already taken
+    // hold INT_MIN, below every key including -inf.  The per-round work stays in
+    // the vector units (the scalar unit is shared by all the waves of the CU):
+    // each lane finds its own first token holding the maximum, the compare mask
+    // is the ballot, the winning lane removes its token, and lane r keeps round
+    // r's entry until the list is written at the end.
     {
       int sk[NC][4];
 #pragma unroll
       for (int c = 0; c < NC; ++c)
 #pragma unroll
         for (int j = 0; j < 4; ++j) sk[c][j] = ((vm >> (c * 4 + j)) & 1u) ? ord_key(kk[c][j]) : INT_MIN;
-      int r = 0;
-      for (; r < K; ++r) {
+      int rk = INT_MIN, ry = INT_MAX;  // lane r: entry r of the wave's list
+      for (int r = 0; r < K; ++r) {
+        int lbc[NC];
         int lb = INT_MIN;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) lb = max(lb, max(max(sk[c][0], sk[c][1]), max(sk[c][2], sk[c][3])));
+        for (int c = 0; c < NC; ++c) {
+          lbc[c] = max(max(sk[c][0], sk[c][1]), max(sk[c][2], sk[c][3]));
+          lb = max(lb, lbc[c]);
+        }
         const int M = wave_max_i(lb);
         if (M == INT_MIN) break;
-        int wy = INT_MAX, wsrc = 0, wbit = 0;
+        // lowest strip, then lowest lane, then lowest position holding M
+        int src = -1, wc = 0;
 #pragma unroll
         for (int c = NC - 1; c >= 0; --c) {
-          unsigned long long mj[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) mj[j] = __ballot(sk[c][j] == M);
-          const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
-          if (any) {
-            const int src = __ffsll((long long)any) - 1;
-            int jj = 3;
-#pragma unroll
-            for (int j = 2; j >= 0; --j) jj = ((mj[j] >> src) & 1ull) ? j : jj;
-            wy = (c * W + wave * 64 + src) * 4 + jj;
-            wsrc = src;
-            wbit = c * 4 + jj;
+          const unsigned long long has = __ballot(lbc[c] == M);
+          if (has) {
+            src = __ffsll((long long)has) - 1;
+            wc = c;
           }
         }
-        if (lane == 0) {
-          w_key[wave][r] = M;
-          w_y[wave][r] = wy;
-        }
+        int jm = 3;  // this lane's first position holding M in strip wc
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+          if (c == wc) {
+            jm = sk[c][2] == M ? 2 : jm;
+            jm = sk[c][1] == M ? 1 : jm;
+            jm = sk[c][0] == M ? 0 : jm;
+          }
+        const int wy = (wc * W + wave * 64 + src) * 4 + __builtin_amdgcn_readlane(jm, src);
+        const int kill = lane == src ? wc * 4 + jm : -1;
 #pragma unroll
         for (int c = 0; c < NC; ++c)
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (wbit == c * 4 + j) sk[c][j] = (lane == wsrc) ? INT_MIN : sk[c][j];
+          for (int j = 0; j < 4; ++j) sk[c][j] = kill == c * 4 + j ? INT_MIN : sk[c][j];
+        rk = lane == r ? M : rk;
+        ry = lane == r ? wy : ry;
       }
-      if (lane == 0)
-        for (; r < K; ++r) w_y[wave][r] = INT_MAX;
+      if (lane < K) {
+        w_key[wave][lane] = rk;
+        w_y[wave][lane] = ry;
+      }
     }
     if (p.traffic && act && g == 0) {
       unsigned long long by = 4ull * V;
