@@ -192,7 +192,10 @@ struct HypState {
   double S;                 // running beam score
 };
 
-template <int W, int NC, int KM, bool AL>
+// MODE: what a launch computes (the code of the other modes is compiled out)
+constexpr int kModeStep = 0, kModeGreedy = 1, kModeBeam = 2;
+
+template <int W, int NC, int KM, bool AL, int MODE>
 __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   constexpr int NW = W / 64;
   constexpr int Vp = NC * 4 * W;
@@ -224,7 +227,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   const int g = threadIdx.x;
   const int wave = g >> 6;
   const int lane = g & 63;
-  const int B = p.B, K = p.k;
+  const int B = MODE == kModeBeam ? p.B : 1, K = p.k;
   const int N = lm.N;
   const int RS = lm.rec_stride;
   // workgroup -> (stream, hypothesis); with xcd_map the B workgroups of a stream
@@ -257,10 +260,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const int V = p.V, blank = p.blank;
     const int sig = p.lm_state[h];
     const int q = p.has_trie ? p.boost_state[h] : 0;
-    const double sc = B > 1 ? p.hyp_score[h] : 0.0;
+    const double sc = MODE == kModeBeam ? p.hyp_score[h] : 0.0;
     const bool ok_lm = sig >= 0 && sig < lm.n_states && sig != blank && (sig != V + 1 || lm.eos_ok);
     const bool ok_q = !p.has_trie || (q >= 0 && q < tr.n_nodes);
-    const bool alive = B == 1 || sc > -INFINITY;
+    const bool alive = MODE != kModeBeam || sc > -INFINITY;
     hs.lmsrc = sig;
     hs.qsrc = q;
     hs.y = -1;
@@ -681,7 +684,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         if (m >= 2) by += 8ull;
         if (p.has_trie) by += 16ull + 16ull * (unsigned long long)dcnt;
       }
-      by += B > 1 ? 8ull : 4ull;
+      by += MODE == kModeBeam ? 8ull : 4ull;
       if (p.fused) by += 4ull * V;
       s_bytes += by;
       s_steps += 1ull;
@@ -754,7 +757,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
         if (!p.has_trie) cq = 0;
       }
-      if (p.step_mode) {
+      if (MODE == kModeStep) {
         if (lane < K) {
           const int64_t o = (int64_t)h * K + lane;
           if (cy == INT_MAX) {
@@ -772,7 +775,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             p.next_boost[o] = q;
           }
         }
-      } else if (B == 1) {
+      } else if (MODE == kModeGreedy) {
         if (lane == 0) {
           p.tokens[(int64_t)t * H + h] = cy;
           const int c1p = hs.c1;
@@ -889,7 +892,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     __syncthreads();
   }
   // ---- final state ----------------------------------------------------------------
-  if (!p.step_mode && g == 0) {
+  if (MODE != kModeStep && g == 0) {
     const int V = p.V;
     int nl = hs.lmsrc, nq = hs.qsrc;
     const int y = hs.y;
@@ -900,7 +903,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     if (moved && nq < 0) nq = tr.root_node[y].w;
     p.lm_state[h] = nl;
     if (p.has_trie) p.boost_state[h] = nq;
-    if (B > 1) p.hyp_score[h] = hs.S;
+    if (MODE == kModeBeam) p.hyp_score[h] = hs.S;
   }
   if (p.traffic && g == 0) {
     const unsigned long long extra = (h == 0 && p.has_trie) ? 4ull * p.V * (unsigned long long)p.T : 0ull;
@@ -918,13 +921,20 @@ __global__ void zero_ints(int *p, int n) {
 // ---------------------------------------------------------------------------
 typedef void (*KernelFn)(Params);
 
+template <int W, int NC, int KM, bool AL>
+KernelFn pick_mode(int mode) {
+  if constexpr (KM == 1) {
+    if (mode == kModeGreedy) return fusion_kernel<W, NC, KM, AL, kModeGreedy>;
+  }
+  return mode == kModeStep ? fusion_kernel<W, NC, KM, AL, kModeStep> : fusion_kernel<W, NC, KM, AL, kModeBeam>;
+}
 template <int W, int NC, int KM>
-KernelFn pick_al(bool al) {
-  return al ? fusion_kernel<W, NC, KM, true> : fusion_kernel<W, NC, KM, false>;
+KernelFn pick_al(bool al, int mode) {
+  return al ? pick_mode<W, NC, KM, true>(mode) : pick_mode<W, NC, KM, false>(mode);
 }
 template <int W, int NC>
-KernelFn pick_k(int km, bool al) {
-  return km == 1 ? pick_al<W, NC, 1>(al) : km == 4 ? pick_al<W, NC, 4>(al) : pick_al<W, NC, 8>(al);
+KernelFn pick_k(int km, bool al, int mode) {
+  return km == 1 ? pick_al<W, NC, 1>(al, mode) : km == 4 ? pick_al<W, NC, 4>(al, mode) : pick_al<W, NC, 8>(al, mode);
 }
 
 struct Shape {
@@ -939,11 +949,11 @@ Shape shape_for(int V) {
   return {1024, 2, 8192};
 }
 
-KernelFn pick(const Shape &sh, int km, bool al) {
-  if (sh.W == 64) return pick_k<64, 1>(km, al);
-  if (sh.W == 256) return pick_k<256, 1>(km, al);
-  if (sh.NC == 1) return pick_k<1024, 1>(km, al);
-  return pick_k<1024, 2>(km, al);
+KernelFn pick(const Shape &sh, int km, bool al, int mode) {
+  if (sh.W == 64) return pick_k<64, 1>(km, al, mode);
+  if (sh.W == 256) return pick_k<256, 1>(km, al, mode);
+  if (sh.NC == 1) return pick_k<1024, 1>(km, al, mode);
+  return pick_k<1024, 2>(km, al, mode);
 }
 
 struct DeviceInfo {
@@ -972,7 +982,8 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   const Shape sh = shape_for(p.V);
   const int km = p.k <= 1 ? 1 : p.k <= 4 ? 4 : 8;
   const bool al = (p.V % 4 == 0) && ((uintptr_t)p.logits % 16 == 0) && (!p.fused || (uintptr_t)p.fused % 16 == 0);
-  KernelFn fn = pick(sh, km, al);
+  const int mode = p.step_mode ? kModeStep : p.B == 1 ? kModeGreedy : kModeBeam;
+  KernelFn fn = pick(sh, km, al, mode);
   const DeviceInfo di = device_info();
   if (!di.ok) return set_error(FUSION_E_HIP, "cannot query the device");
   const size_t dyn = (size_t)4 * (2 * sh.Vp + 3 * kAux + 4);
