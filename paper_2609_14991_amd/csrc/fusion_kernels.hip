@@ -59,6 +59,7 @@ constexpr int kNodeLane = 32;                 // lanes 32..35 of the record word
 constexpr int kSpinLimit = 1 << 20;           // bounded wait at the beam rendezvous (polls, ~1 s)
 
 __device__ int g_status;
+__device__ int32_t g_zero_words[4];  // never written: read by lanes that have no record word
 
 struct Params {
   LMDevice lm;
@@ -93,7 +94,13 @@ __device__ __forceinline__ unsigned long long umin64(unsigned long long a, unsig
 // byte offset; reads past the row return 0
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
 __device__ __forceinline__ rsrc_t row_rsrc(const float *base, int n) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float *>(base), (short)0, n * 4, 0x00020000);
+  // every field uniform (a descriptor the compiler cannot prove uniform costs a
+  // readfirstlane loop around each access)
+  const unsigned long long v = reinterpret_cast<unsigned long long>(base);
+  const unsigned lo = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)v);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readfirstlane((int)(unsigned)(v >> 32));
+  float *ub = reinterpret_cast<float *>(((unsigned long long)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0, __builtin_amdgcn_readfirstlane(n * 4), 0x00020000);
 }
 __device__ __forceinline__ float4 row_load4(rsrc_t r, int voff, int soff) {
   return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
@@ -328,21 +335,38 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     }
     const int4 *np = nullptr;
     if (ok && p.has_trie) np = qsrc < 0 ? tr.root_node + yin : tr.node + qsrc;
-    int rw = 0;  // lanes 0..RS-1: record words; lanes 32..35: phrase node
-    if (rp && lane < RS) rw = rp[lane];
-    if (np && lane >= kNodeLane && lane < kNodeLane + 4) rw = reinterpret_cast<const int *>(np)[lane - kNodeLane];
     const int64_t rowoff = ((int64_t)t * H + h) * V;
+    // this frame's logits (fetched during the previous frame); waited for here,
+    // before this frame's loads are issued
+#pragma unroll
+    for (int c = 0; c < NC; ++c) asm volatile("" ::"v"(xraw[c][0]), "v"(xraw[c][1]), "v"(xraw[c][2]), "v"(xraw[c][3]));
     float xv[NC][4];
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j) xv[c][j] = (act && (c * W + g) * 4 + j < V) ? xraw[c][j] : -INFINITY;
-    if (t + 1 < p.T) fetch_logits(t + 1);
+    // lanes 0..RS-1: record words; lanes 32..35: phrase node; every other lane,
+    // and every lane without a record or node, reads a zero word.  One load per
+    // lane, used as loaded, so that decoding the record waits for it alone and not
+    // for the dense row and the logits fetched after it
+    int rw;
+    {
+      const int32_t *src = &g_zero_words[0];
+      if (rp && lane < RS) src = rp + lane;
+      if (np && lane >= kNodeLane && lane < kNodeLane + 4) src = reinterpret_cast<const int *>(np) + (lane - kNodeLane);
+      rw = *src;
+    }
+    // unconditional (the last frame fetches its own row again): a conditional
+    // fetch would make the compiler wait for it where the branches join
+    fetch_logits(min(t + 1, p.T - 1));
     // the initial state of a run may need its record to learn c_1
     if (ok && c1 < 0) c1 = rp ? (rdl(rw, 0) & 0xFFFF) : lmsrc;
-    // level-1 dense row straight into the LDS LM row; arcs scattered later overwrite it
-    if (ok) {
-      const float *drow = lm.dense + (int64_t)c1 * V;
+    // level-1 dense row straight into the LDS LM row; arcs scattered later overwrite
+    // it.  Issued unconditionally (row 0 stands in when the hypothesis has no keys
+    // to compute this frame), so that the record decode can wait for the record
+    // alone
+    {
+      const float *drow = lm.dense + (int64_t)(ok ? c1 : 0) * V;
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
         const int wbase = c * W + wave * 64;  // first 4-token strip of this wave

@@ -300,3 +300,34 @@ def test_repeat_runs_are_identical(c2):
         res.append((out["tokens"].cpu(), out["parents"].cpu(), out["fused"].cpu(), ls.cpu(), sc.cpu()))
     for a, b in zip(*res):
         assert torch.equal(a, b)
+
+
+def test_beam_in_several_launch_batches():
+    """More streams than the device holds at once (160 x 4 workgroups of 1024
+    lanes): the run is split into launch batches whose rendezvous buffers are
+    cleared in between.  Every decision is replayed by the oracle."""
+    rng = np.random.default_rng(80)
+    V, S, B, k, T = 1100, 160, 4, 4, 12
+    lm = tiny_random_lm(rng, V, 4, n_sent=3000)
+    ph = tiny_random_phrases(rng, V, n=40, max_len=4, alphabet=min(V - 1, 30), with_completion=True)
+    glm, gtr = F.ngram_load_arrays(lm), F.boost_build_phrases(V, 0, ph)
+    olm, otr = oracle.OracleLM(lm), oracle.OracleTrie(V, 0, ph)
+    x = (rng.standard_normal((T, S * B, V)) * 2).astype(np.float32)
+    x[:, :, 0] += 2
+    H = S * B
+    ls = torch.full((H,), V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev())
+    sc0 = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)
+    sc = torch.from_numpy(sc0.copy()).to(dev())
+    out = F.run(glm, gtr, torch.from_numpy(x).to(dev()), S, B, k, 0.5, 0.5, 0, F.FUSION_BLANK_COMPETE, ls, bs, sc)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.run(olm, otr, x, S, B, k, 0.5, 0.5, 0, 1, [V] * H, [0] * H, sc0,
+                   forced_tokens=out["tokens"].cpu().numpy(), forced_parents=out["parents"].cpu().numpy(),
+                   tol=TIE_TOL, threads=8)
+    assert (r["mismatch_at"] < 0).all()
+    assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
+    assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
+    fin = np.isfinite(r["hyp_score"])
+    assert np.array_equal(np.isfinite(sc.cpu().numpy()), fin)
+    assert np.abs(sc.cpu().numpy()[fin] - r["hyp_score"][fin]).max() <= T * SCORE_TOL
