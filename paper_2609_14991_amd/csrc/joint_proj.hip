@@ -12,8 +12,8 @@
 // tiles (64 fp32 accumulators per lane).  K advances in stages of BK: every
 // lane fetches its 16-byte strips of A and W for the next stage into registers
 // while the current stage, double-buffered in LDS (rows padded by 16 bytes),
-// feeds the MFMAs.  Tiles are numbered column-fastest, so with the hardware's
-// round-robin of workgroups over the 8 XCDs each XCD's L2 holds a quarter of W.
+// feeds the MFMAs.  Tiles are assigned per XCD (see the kernel) so that each
+// XCD's L2 serves a row band of A to eight column tiles and keeps half of W.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -37,7 +37,7 @@ template <int kWM, int kWN, int kBK>
 __global__ void __launch_bounds__(64 * kWM * kWN) joint_proj_kernel(const uint16_t *__restrict__ A,
                                                                      const uint16_t *__restrict__ W,
                                                                      const float *__restrict__ bias, int M, int N,
-                                                                     int K, int n_col_tiles, int vec_out,
+                                                                     int K, int n_col_tiles, int xcd_map, int vec_out,
                                                                      float *__restrict__ out) {
   constexpr int kBM = 64 * kWM, kBN = 64 * kWN;
   constexpr int kLd = kBK + 8;  // bf16 per LDS row (16-byte pad)
@@ -50,8 +50,22 @@ __global__ void __launch_bounds__(64 * kWM * kWN) joint_proj_kernel(const uint16
   uint16_t(*sA)[kBM * kLd] = reinterpret_cast<uint16_t(*)[kBM * kLd]>(smem);
   uint16_t(*sW)[kBN * kLd] = reinterpret_cast<uint16_t(*)[kBN * kLd]>(smem + 2 * kBM * kLd);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int tile = blockIdx.x;
-  const int bn = (tile % n_col_tiles) * kBN, bm = (tile / n_col_tiles) * kBM;
+  // tile of this workgroup.  With xcd_map (row tiles a multiple of 4, column
+  // tiles even) workgroup w runs on XCD w % 8 under the hardware's round-robin,
+  // and XCD x takes the row tiles = x % 4 (mod 4) against column half x / 4: a
+  // row band of A is fetched by two XCDs instead of eight and each XCD's L2
+  // keeps half of W.  Otherwise tiles go column-fastest.
+  int tr, tc;
+  if (xcd_map) {
+    const int x = blockIdx.x & 7, i = blockIdx.x >> 3;
+    const int half = n_col_tiles >> 1;
+    tr = (i / half) * 4 + (x & 3);
+    tc = (x >> 2) * half + i % half;
+  } else {
+    tr = blockIdx.x / n_col_tiles;
+    tc = blockIdx.x % n_col_tiles;
+  }
+  const int bn = tc * kBN, bm = tr * kBM;
   const int wm = (wave / kWN) * 64, wn = (wave % kWN) * 64;
 
   // reads past a row range or past K return zeros (buffer range check)
@@ -193,8 +207,9 @@ extern "C" int joint_project(const uint16_t *A, const uint16_t *W, const float *
   if ((int64_t)nct * nrt > 0x7FFFFFFFll) return set_error(FUSION_E_UNSUPPORTED, "too many tiles");
   // whole 16-byte row segments when every row starts 16-byte aligned
   const int vec_out = (N % 4 == 0 && (uintptr_t)out % 16 == 0) ? 1 : 0;
+  const int xcd_map = (nrt % 4 == 0 && nct % 2 == 0) ? 1 : 0;
   hipLaunchKernelGGL((joint_proj_kernel<WM, WN, BK>), dim3(nct * nrt), dim3(64 * WM * WN), 0, stream, A, W, bias, M,
-                     N, K, nct, vec_out, out);
+                     N, K, nct, xcd_map, vec_out, out);
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? FUSION_OK : hip_error(e, "joint projection launch");
 }
