@@ -119,7 +119,10 @@ class NgramTables:
 
     def __del__(self):
         if getattr(self, "h", None) is not None and self.h.value:
-            lib().ngram_free(self.h)
+            try:
+                lib().ngram_free(self.h)
+            except Exception:  # interpreter shutdown: the module may be gone
+                pass
             self.h = None
 
 
@@ -132,7 +135,10 @@ class BoostTrie:
 
     def __del__(self):
         if getattr(self, "h", None) is not None and self.h.value:
-            lib().boost_free(self.h)
+            try:
+                lib().boost_free(self.h)
+            except Exception:  # interpreter shutdown: the module may be gone
+                pass
             self.h = None
 
 

@@ -294,7 +294,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   __syncthreads();
 
   // logits strip of this lane, raw (masked per frame): frame t+1's strip is
-  // fetched at the start of frame t, so it is in registers when t+1 begins
+  // fetched during frame t, so it is in registers when t+1 begins
   const int voff = g * 16;
   float xraw[NC][4];
   auto fetch_logits = [&](int tt) {
@@ -356,9 +356,6 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       if (np && lane >= kNodeLane && lane < kNodeLane + 4) src = reinterpret_cast<const int *>(np) + (lane - kNodeLane);
       rw = *src;
     }
-    // unconditional (the last frame fetches its own row again): a conditional
-    // fetch would make the compiler wait for it where the branches join
-    fetch_logits(min(t + 1, p.T - 1));
     // the initial state of a run may need its record to learn c_1
     if (ok && c1 < 0) c1 = rp ? (rdl(rw, 0) & 0xFFFF) : lmsrc;
     // level-1 dense row straight into the LDS LM row; arcs scattered later overwrite
@@ -642,6 +639,11 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
       }
     }
+    // the next frame's logits strip: fetched here, in a compute-bound phase, rather
+    // than beside the frame-start loads, whose burst sets the start of the frame.
+    // Unconditional (the last frame fetches its own row again): a conditional
+    // fetch would make the compiler wait for it where the branches join
+    fetch_logits(min(t + 1, p.T - 1));
     // ---- the wave's top-k: per round the wave maximum of the remaining keys, then
     // the lowest id holding it (ties to the lowest id).  Keys compete as
     // order-preserving ints; tokens that are not candidates or are already taken
