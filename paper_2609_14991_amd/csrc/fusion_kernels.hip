@@ -209,10 +209,16 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   constexpr int kUA = W >= 1024 ? 1 : 4;  // arcs per lane fetched in the second hop
   constexpr int kUD = W >= 1024 ? 1 : 2;  // phrase transitions per lane fetched in the second hop
   extern __shared__ __align__(16) unsigned char dyn[];
+  // LDS rows, one entry per token: the dense level-1 LM row; the winning explicit
+  // arc (stamp << 48 | level << 45 | offset << 32 | value bits, kept by an atomic
+  // max, so the highest level wins whatever the order of the writes); the phrase
+  // transition overriding the root's (stamp << 16 | transition + 1).  The stamp
+  // is the frame's (t mod 2^15) + 1: entries of earlier frames compare lower and
+  // read as absent, so no per-frame clearing is needed
   float *lmval = reinterpret_cast<float *>(dyn);
-  uint32_t *win = reinterpret_cast<uint32_t *>(dyn) + Vp;
-  uint16_t *win16 = reinterpret_cast<uint16_t *>(win);
-  float *sE = reinterpret_cast<float *>(dyn) + 2 * Vp;  // sE[j + 1]: entry value of transition j
+  unsigned long long *arcw = reinterpret_cast<unsigned long long *>(dyn + 4 * Vp);
+  uint32_t *ptag = reinterpret_cast<uint32_t *>(dyn + 12 * Vp);
+  float *sE = reinterpret_cast<float *>(dyn + 16 * Vp);  // sE[j + 1]: entry value of transition j
   int *sDT = reinterpret_cast<int *>(sE + kAux + 4);
   int *sTN = sDT + kAux;
   __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves];
@@ -232,6 +238,16 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   const LMDevice &lm = p.lm;
   const TrieDevice &tr = p.tr;
   const int g = threadIdx.x;
+  // this lane's entries of the arc and phrase rows back to 0 (absent)
+  auto clear_rows = [&]() {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int y0 = (c * W + g) * 4;
+      *reinterpret_cast<uint4 *>(arcw + y0) = make_uint4(0u, 0u, 0u, 0u);
+      *reinterpret_cast<uint4 *>(arcw + y0 + 2) = make_uint4(0u, 0u, 0u, 0u);
+      *reinterpret_cast<uint4 *>(ptag + y0) = make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
   const int wave = g >> 6;
   const int lane = g & 63;
   const int B = MODE == kModeBeam ? p.B : 1, K = p.k;
@@ -289,8 +305,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const int y0 = (c * W + g) * 4;
 #pragma unroll
     for (int j = 0; j < 4; ++j) rE[c][j] = (p.has_trie && y0 + j < p.V) ? tr.root_E[y0 + j] : 0.0f;
-    *reinterpret_cast<uint4 *>(win + y0) = make_uint4(0u, 0u, 0u, 0u);
   }
+  clear_rows();
   __syncthreads();
 
   // logits strip of this lane, raw (masked per frame): frame t+1's strip is
@@ -319,11 +335,12 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const bool act = (fl & 1) != 0;
     const bool inv = act && (fl & 2) != 0;
     const bool ok = act && !inv;
-    // the tag words of the previous frame (its winners read them before its last
-    // barrier) are cleared before this frame's scatter
-    if (t > 0) {
-#pragma unroll
-      for (int c = 0; c < NC; ++c) *reinterpret_cast<uint4 *>(win + (c * W + g) * 4) = make_uint4(0u, 0u, 0u, 0u);
+    // stamps repeat every 2^15 frames: the rows are cleared before they would
+    // (the previous frame's last reads of them precede its final barrier)
+    const uint32_t stamp = (uint32_t)(t & 0x7FFF) + 1u;
+    if (stamp == 1u && t > 0) {
+      clear_rows();
+      __syncthreads();
     }
     const int lmsrc = uni(hs.lmsrc), qsrc = uni(hs.qsrc), yin = uni(hs.y);
     int c1 = uni(hs.c1);
@@ -485,9 +502,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 #pragma unroll
       for (int L = 2; L < kMaxLevels; ++L) s_lbeg[L] = lbeg[L];
     }
-    __builtin_amdgcn_s_waitcnt(0);  // the dense row has landed in LDS
-    __syncthreads();
-    // ---- scatter ------------------------------------------------------------------
+    // ---- scatter (no ordering between levels: see arcw) ----------------------------
     // an arc of level L is stored summed with the backoffs of levels L+1.., the
     // addition order of the backoff recursion
     auto put_arc = [&](int L, int j, int2 a, int tnext) {
@@ -496,8 +511,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         float v = as_float(a.y);
 #pragma unroll
         for (int L2 = 3; L2 < kMaxLevels; ++L2) v = v + (L2 > L ? bo[L2] : 0.0f);
-        lmval[y] = v;
-        win16[2 * y] = (uint16_t)((L << 13) | j);
+        const uint32_t tag = (stamp << 16) | (uint32_t)((L << 13) | j);
+        __hip_atomic_fetch_max(arcw + y, ((unsigned long long)tag << 32) | (unsigned long long)__float_as_uint(v),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         if (L == N - 1 && j < kAux) sTN[j] = tnext;
       }
     };
@@ -506,7 +522,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       for (int u = 0; u < kUD; ++u) {
         const int j = u * W + g;
         if (j < dcnt) {
-          win16[2 * dd[u].x + 1] = (uint16_t)(j + 1);
+          ptag[dd[u].x] = (stamp << 16) | (uint32_t)(j + 1);
           if (j < kAux) {
             sE[j + 1] = as_float(dd[u].z);
             sDT[j] = dd[u].y;
@@ -515,21 +531,18 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
       for (int j = kUD * W + g; j < dcnt; j += W) {
         const int4 e = tr.delta[dbeg + j];
-        win16[2 * e.x + 1] = (uint16_t)(j + 1);
+        ptag[e.x] = (stamp << 16) | (uint32_t)(j + 1);
         if (j < kAux) {
           sE[j + 1] = as_float(e.z);
           sDT[j] = e.y;
         }
       }
-    }
-    const int nphase = N - 2 > 1 ? N - 2 : 1;
-    int covered = kUA * W;  // flattened arcs already fetched
-    for (int ph = 0; ph < nphase; ++ph) {
-      const int L = ph + 2;
-      if (ok && L <= m) {
 #pragma unroll
-        for (int u = 0; u < kUA; ++u)
-          if ((at[u] >> 16) == L) put_arc(L, at[u] & 0xFFFF, ab[u], tn[u]);
+      for (int u = 0; u < kUA; ++u)
+        if (at[u] != 0) put_arc(at[u] >> 16, at[u] & 0xFFFF, ab[u], tn[u]);
+      // arcs beyond the first kUA * W of the flattened levels
+      int covered = kUA * W;
+      for (int L = 2; L <= m; ++L) {
         const int bL = rdl(rw, rec_beg_lane(L)), cL = rdl(rw, rec_cnt_lane(L));
         const int done = min(cL, max(0, covered));
         covered -= cL;
@@ -550,8 +563,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           }
         }
       }
-      __syncthreads();
     }
+    __builtin_amdgcn_s_waitcnt(0);  // the dense row has landed in LDS
+    __syncthreads();
     // ---- combine the row statistics (lanes 0..NW-1 hold one wave each) --------------
     float lse;
     int am;
@@ -591,37 +605,48 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         kk[c][j] = xv[c][j];
       }
       if (want_keys) {
-        const uint4 w4 = *reinterpret_cast<const uint4 *>(win + y0);
+        const uint4 p4 = *reinterpret_cast<const uint4 *>(ptag + y0);
+        const uint4 a01 = *reinterpret_cast<const uint4 *>(arcw + y0);
+        const uint4 a23 = *reinterpret_cast<const uint4 *>(arcw + y0 + 2);
         const float4 l4 = *reinterpret_cast<const float4 *>(lmval + y0);
-        const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
+        const uint32_t aw[4] = {a01.y, a01.w, a23.y, a23.w};  // tag halves of the arc entries
+        const uint32_t av[4] = {a01.x, a01.z, a23.x, a23.z};  // value halves
         const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        // transition + 1 of this frame's phrase entry, 0 if none
+        uint32_t hi[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t pw = j == 0 ? p4.x : j == 1 ? p4.y : j == 2 ? p4.z : p4.w;
+          hi[j] = (pw >> 16) == stamp ? (pw & 0xFFFFu) : 0u;
+        }
         // the phrase entry values: the LDS copy of the state's first kAux transitions
         // (read for every token, index 0 when unused, so that no per-token branch
         // guards the read), the delta table beyond them only for a state with more
         float eh[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) eh[j] = sE[min((int)(ww[j] >> 16), kAux)];
+        for (int j = 0; j < 4; ++j) eh[j] = sE[min((int)hi[j], kAux)];
         asm volatile("" ::"v"(eh[0]), "v"(eh[1]), "v"(eh[2]), "v"(eh[3]));
         if (dcnt > kAux) {
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int hi = (int)(ww[j] >> 16);
-            if (hi > kAux) eh[j] = as_float(tr.delta[dbeg + hi - 1].z);
-          }
+          for (int j = 0; j < 4; ++j)
+            if (hi[j] > (uint32_t)kAux) eh[j] = as_float(tr.delta[dbeg + (int)hi[j] - 1].z);
+        }
+        // the dense row plus the backoffs of levels 2..m in increasing order (the
+        // levels above m back off by 0)
+        float dres[4] = {lv[0], lv[1], lv[2], lv[3]};
+        for (int L2 = 2; L2 <= m; ++L2) {
+          const float b2 = as_float(rdl(rw, rec_bo_lane(L2)));
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dres[j] = dres[j] + b2;
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int y = y0 + j;
           const float x = xv[c][j];
-          const uint32_t lo = ww[j] & 0xFFFFu, hi = ww[j] >> 16;
-          // LM: the scattered value if an arc won, else the dense row plus the
-          // backoffs of levels 2.. in increasing order
-          float dres = lv[j];
-#pragma unroll
-          for (int L2 = 2; L2 < kMaxLevels; ++L2) dres = dres + bo[L2];
-          const float lmv = lo ? lv[j] : dres;
+          // LM: this frame's winning arc if there is one, else the backed-off dense row
+          const float lmv = (aw[j] >> 16) == stamp ? __uint_as_float(av[j]) : dres[j];
           // phrases: the transition's entry value if this state overrides y, else the root's
-          const float e = hi ? eh[j] : rE[c][j];
+          const float e = hi[j] ? eh[j] : rE[c][j];
           const float bst = e - phiq;
           const float a1 = p.lam * lmv;
           const float a2 = x + a1;
@@ -762,9 +787,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       const float cf = cy != INT_MAX ? key_of(ck) - lse : -INFINITY;
       int cl = sid, cq = qid;
       if (cy != INT_MAX && cy != blank) {
-        // the token's LDS tag word: LM winner level / offset, phrase transition
-        const uint32_t cw = win[cy];
-        const uint32_t lo = cw & 0xFFFFu, hi = cw >> 16;
+        // the token's LDS entries of this frame: LM winner level / offset, phrase transition
+        const uint32_t aw = (uint32_t)(arcw[cy] >> 32), pw = ptag[cy];
+        const uint32_t lo = (aw >> 16) == stamp ? (aw & 0xFFFFu) : 0u;
+        const uint32_t hi = (pw >> 16) == stamp ? (pw & 0xFFFFu) : 0u;
         cl = -1;
         if (lo) {
           const int L = (int)(lo >> 13), jj = (int)(lo & 0x1FFFu);
@@ -1012,7 +1038,7 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   KernelFn fn = pick(sh, km, al, mode);
   const DeviceInfo di = device_info();
   if (!di.ok) return set_error(FUSION_E_HIP, "cannot query the device");
-  const size_t dyn = (size_t)4 * (2 * sh.Vp + 3 * kAux + 4);
+  const size_t dyn = (size_t)4 * (4 * sh.Vp + 3 * kAux + 4);
   hipFuncAttributes attr;
   hipError_t e = hipFuncGetAttributes(&attr, reinterpret_cast<const void *>(fn));
   if (e != hipSuccess) return hip_error(e, "hipFuncGetAttributes");

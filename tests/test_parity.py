@@ -135,6 +135,33 @@ def test_c2_stream_in_13_frame_chunks(c2):
     assert int(ls.cpu()[0]) == r["lm_state"][0] and int(bs.cpu()[0]) == r["boost_state"][0]
 
 
+def test_long_run_past_the_lds_stamp_period():
+    """One launch of 33068 frames: the LDS rows of explicit arcs and phrase
+    transitions carry a frame stamp that repeats every 32768 frames, so the run
+    crosses the point where they are cleared; every token and the final states
+    equal the oracle's."""
+    rng = np.random.default_rng(91)
+    V, S, T = 300, 2, 32768 + 300
+    lm = tiny_random_lm(rng, V, 4, n_sent=2000)
+    ph = tiny_random_phrases(rng, V, n=30, max_len=4, alphabet=20, with_completion=True)
+    glm, gtr = F.ngram_load_arrays(lm), F.boost_build_phrases(V, 0, ph)
+    olm, otr = oracle.OracleLM(lm), oracle.OracleTrie(V, 0, ph)
+    x = (rng.standard_normal((T, S, V)) * 2).astype(np.float32)
+    x[:, :, 0] += 2
+    ls = torch.full((S,), V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((S,), dtype=torch.int32, device=dev())
+    out = F.run(glm, gtr, torch.from_numpy(x).to(dev()), S, 1, 1, 0.5, 0.5, 0, F.FUSION_BLANK_AM, ls, bs)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.run(olm, otr, x, S, 1, 1, 0.5, 0.5, 0, 0, [V] * S, [0] * S, threads=2)
+    tok = out["tokens"].cpu().numpy()
+    assert (tok[32768:] != 0).sum() > 100  # states keep moving after the wrap
+    bad = np.argwhere(tok != r["tokens"])
+    assert bad.size == 0, f"first mismatch (frame, stream) {bad[0]}"
+    assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
+    assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
+
+
 def test_c3_batched_greedy_prefix():
     """C3 (64 streams, 10% peaked rows): the first 60 frames of every stream."""
     w = load_workload(3, T=60)
