@@ -191,6 +191,12 @@ __device__ __forceinline__ void row_best(float &k, int &y) {
   dpp_best<0x140>(k, y);
 }
 
+// Barrier for data exchanged through LDS alone: waits for this wave's LDS
+// operations but not for its vector-memory loads in flight (the next frame's
+// logits).  __syncthreads would wait for those too (its release fence waits for
+// every outstanding vector-memory operation).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // hypothesis state carried between frames (LDS, written by one lane)
 struct HypState {
   int lmsrc, qsrc, y, c1p;  // where the state comes from (see TopK), token, parent's c_1
@@ -313,20 +319,95 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   // fetched during frame t, so it is in registers when t+1 begins
   const int voff = g * 16;
   float xraw[NC][4];
-  auto fetch_logits = [&](int tt) {
-    const rsrc_t xr = row_rsrc(p.logits + ((int64_t)tt * H + h) * p.V, p.V);
+  float xraw0[NC][4];  // wave 1: wave 0's strip too, for its row statistics
+  auto fetch_strip = [&](const rsrc_t &xr, float (&dst)[NC][4], int off) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       if (AL) {
-        const float4 xx = row_load4(xr, voff, c * W * 16);
-        xraw[c][0] = xx.x; xraw[c][1] = xx.y; xraw[c][2] = xx.z; xraw[c][3] = xx.w;
+        const float4 xx = row_load4(xr, off, c * W * 16);
+        dst[c][0] = xx.x; dst[c][1] = xx.y; dst[c][2] = xx.z; dst[c][3] = xx.w;
       } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) xraw[c][j] = row_load1(xr, voff + 4 * j, c * W * 16);
+        for (int j = 0; j < 4; ++j) dst[c][j] = row_load1(xr, off + 4 * j, c * W * 16);
       }
     }
   };
+  auto fetch_logits = [&](int tt) {
+    const rsrc_t xr = row_rsrc(p.logits + ((int64_t)tt * H + h) * p.V, p.V);
+    fetch_strip(xr, xraw, voff);
+    if (NW > 1 && wave == 1) fetch_strip(xr, xraw0, lane * 16);
+  };
   fetch_logits(0);
+  // row statistics of the logits of strip sw (the 64-lane strip of wave sw) held
+  // in xs: strip max, sum of exp below it, lowest id holding the max (only the
+  // acoustic blank decision needs it).  They depend on the logits alone, so those
+  // of frame t+1 are computed in frame t by the waves that are otherwise idle
+  // while wave 0 ends the frame (wave 1 takes wave 0's strip); frame 0's here
+  auto row_stats = [&](const float (&xs)[NC][4], int sw, int V) {
+    float xv[NC][4];
+    int xo[NC][4];  // order-preserving images of the logits (tokens >= V: -inf)
+    int lmx = INT_MIN;
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        xv[c][j] = (c * W + sw * 64 + lane) * 4 + j < V ? xs[c][j] : -INFINITY;
+        xo[c][j] = ord_key(xv[c][j]);
+        lmx = max(lmx, xo[c][j]);
+      }
+    const int mwo = wave_max_i(lmx);
+    const float mw = key_of(mwo);
+    float lsum = 0.0f;
+    if (mw > -INFINITY) {
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) lsum += (xv[c][j] > -INFINITY) ? exp_fast(xv[c][j] - mw) : 0.0f;
+    }
+    const float ssum = wave_sum(lsum);
+    int aid = INT_MAX;
+    if (p.mode == FUSION_BLANK_AM && mw > -INFINITY) {
+#pragma unroll
+      for (int c = NC - 1; c >= 0; --c) {
+        unsigned long long mj[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) mj[j] = __ballot(xo[c][j] == mwo && (c * W + sw * 64 + lane) * 4 + j < V);
+        const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
+        if (any) {
+          const int src = __ffsll((long long)any) - 1;
+          int jj = 3;
+#pragma unroll
+          for (int j = 2; j >= 0; --j) jj = ((mj[j] >> src) & 1ull) ? j : jj;
+          aid = (c * W + sw * 64 + src) * 4 + jj;
+        }
+      }
+    }
+    if (lane == 0) {
+      s_pm[sw] = mw;
+      s_ps[sw] = ssum;
+      s_paid[sw] = aid;
+    }
+  };
+  // the level-1 dense row of context token cc straight into the LDS LM row (this
+  // wave's strips)
+  auto load_dense = [&](int cc, int V) {
+    const float *drow = lm.dense + (int64_t)cc * V;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int wbase = c * W + wave * 64;  // first 4-token strip of this wave
+      if (AL) {
+        const int y0 = (wbase + lane) * 4;
+        __builtin_amdgcn_global_load_lds(drow + (y0 < V ? y0 : 0), (lds_ptr_t)(lmval + wbase * 4), 16, 0, 0);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int y = wbase * 4 + j * 64 + lane;
+          __builtin_amdgcn_global_load_lds(drow + (y < V ? y : 0), (lds_ptr_t)(lmval + wbase * 4 + j * 64), 4, 0, 0);
+        }
+      }
+    }
+  };
+  row_stats(xraw, wave, p.V);
 
   bool aborted = false;  // after one failed rendezvous this workgroup stops waiting
   for (int t = 0; t < p.T; ++t) {
@@ -375,73 +456,11 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     }
     // the initial state of a run may need its record to learn c_1
     if (ok && c1 < 0) c1 = rp ? (rdl(rw, 0) & 0xFFFF) : lmsrc;
-    // level-1 dense row straight into the LDS LM row; arcs scattered later overwrite
-    // it.  Issued unconditionally (row 0 stands in when the hypothesis has no keys
-    // to compute this frame), so that the record decode can wait for the record
-    // alone
-    {
-      const float *drow = lm.dense + (int64_t)(ok ? c1 : 0) * V;
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        const int wbase = c * W + wave * 64;  // first 4-token strip of this wave
-        if (AL) {
-          const int y0 = (wbase + lane) * 4;
-          __builtin_amdgcn_global_load_lds(drow + (y0 < V ? y0 : 0), (lds_ptr_t)(lmval + wbase * 4), 16, 0, 0);
-        } else {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int y = wbase * 4 + j * 64 + lane;
-            __builtin_amdgcn_global_load_lds(drow + (y < V ? y : 0), (lds_ptr_t)(lmval + wbase * 4 + j * 64), 4, 0, 0);
-          }
-        }
-      }
-    }
-    // ---- row statistics: wave max, sum of exp below it, raw argmax (while the
-    // state record is in flight) -------------------------------------------------
-    {
-      int xo[NC][4];  // order-preserving images of the logits (excluded tokens: -inf)
-      int lmx = INT_MIN;
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          xo[c][j] = ord_key(xv[c][j]);
-          lmx = max(lmx, xo[c][j]);
-        }
-      const int mwo = wave_max_i(lmx);
-      const float mw = key_of(mwo);
-      float lsum = 0.0f;
-      if (mw > -INFINITY) {
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) lsum += (xv[c][j] > -INFINITY) ? exp_fast(xv[c][j] - mw) : 0.0f;
-      }
-      const float sw = wave_sum(lsum);
-      // lowest id holding the wave max (only the acoustic blank decision needs it)
-      int aid = INT_MAX;
-      if (p.mode == FUSION_BLANK_AM && mw > -INFINITY) {
-#pragma unroll
-        for (int c = NC - 1; c >= 0; --c) {
-          unsigned long long mj[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) mj[j] = __ballot(xo[c][j] == mwo && (c * W + g) * 4 + j < V);
-          const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
-          if (any) {
-            const int src = __ffsll((long long)any) - 1;
-            int jj = 3;
-#pragma unroll
-            for (int j = 2; j >= 0; --j) jj = ((mj[j] >> src) & 1ull) ? j : jj;
-            aid = (c * W + wave * 64 + src) * 4 + jj;
-          }
-        }
-      }
-      if (lane == 0) {
-        s_pm[wave] = mw;
-        s_ps[wave] = sw;
-        s_paid[wave] = aid;
-      }
-    }
+    // level-1 dense row straight into the LDS LM row.  Issued unconditionally
+    // (row 0 stands in when the hypothesis has no keys to compute this frame), so
+    // that the record decode can wait for the record alone
+    load_dense(ok ? c1 : 0, V);
+    if (NW == 1 && t > 0) row_stats(xraw, 0, V);  // a single wave has no idle helper
     // ---- decode the record ------------------------------------------------------
     // (words a record does not use, the levels above m among them, read as 0, as do
     // the node lanes without a node)
@@ -740,7 +759,12 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       s_bytes += by;
       s_steps += 1ull;
     }
-    __syncthreads();
+    lds_barrier();
+    // the next frame's row statistics
+    if (NW > 1 && wave != 0 && t + 1 < p.T) {
+      row_stats(xraw, wave, V);
+      if (wave == 1) row_stats(xraw0, 0, V);
+    }
     // ---- the hypothesis' top-k (wave 0): the K-entry lists of the NW waves spread
     // over the lanes (entry j of wave w is element e = j*NW + w, lane e % 64, slot
     // e / 64); K rounds of a wave maximum, ties to the lowest id -------------------
@@ -829,8 +853,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
       } else if (MODE == kModeGreedy) {
         if (lane == 0) {
-          p.tokens[(int64_t)t * H + h] = cy;
           const int c1p = hs.c1;
+          p.tokens[(int64_t)t * H + h] = cy;
           hs.lmsrc = cl;
           hs.qsrc = cq;
           hs.y = cy;
@@ -941,7 +965,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
       }
     }
-    __syncthreads();
+    lds_barrier();
   }
   // ---- final state ----------------------------------------------------------------
   if (MODE != kModeStep && g == 0) {
