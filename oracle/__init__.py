@@ -87,6 +87,14 @@ def lib():
         L.or_run.argtypes = [vp, vp, f32p, c_int, c_int, c_int, c_int, c_int, c_float, c_float,
                              c_int, c_int, i32p, i32p, f64p, i32p, i32p, f64p, i32p, i32p, f64p,
                              i32p, i32p, c_double, i64p, i64p, c_int]
+        L.or_step_lms.restype = c_int
+        L.or_step_lms.argtypes = [ctypes.POINTER(vp), f32p, c_int, vp, f32p, i32p, i32p, c_int,
+                                  c_int, c_float, c_int, c_int, c_int, f32p, f64p, f64p, i32p,
+                                  f64p, i32p, i32p]
+        L.or_run_lms.restype = c_int
+        L.or_run_lms.argtypes = [ctypes.POINTER(vp), f32p, c_int, vp, f32p, c_int, c_int, c_int,
+                                 c_int, c_int, c_float, c_int, c_int, i32p, i32p, f64p, i32p, i32p,
+                                 f64p, i32p, i32p, f64p, i32p, i32p, c_double, i64p, i64p, c_int]
         _lib = L
     return _lib
 
@@ -274,6 +282,85 @@ def run(lm: OracleLM, trie: OracleTrie | None, logits, S, B, k, lam, beta, blank
                       _p(lo, ctypes.c_int32), _p(bo, ctypes.c_int32), _p(so, ctypes.c_double),
                       _p(ft, ctypes.c_int32), _p(fp, ctypes.c_int32), float(tol),
                       _p(near, ctypes.c_int64), _p(mis, ctypes.c_int64), int(threads))
+    if rc != 0:
+        raise OracleError(_err())
+    return dict(tokens=tok, parents=par, sel_score=sel, lm_state=lo, boost_state=bo,
+                hyp_score=so if B > 1 else None, near_ties=near[:S], mismatch_at=mis[:S])
+
+
+MAX_LMS = 4
+
+
+def _lm_list(lms, alphas):
+    lms, alphas = list(lms), [float(a) for a in alphas]
+    if not 1 <= len(lms) <= MAX_LMS or len(alphas) != len(lms):
+        raise OracleError("need 1..4 LMs and one weight per LM")
+    hs = (ctypes.c_void_p * len(lms))(*[m.h for m in lms])
+    return hs, np.array(alphas, dtype=np.float32), len(lms)
+
+
+def step_lms(lms, alphas, trie: OracleTrie | None, logits, lm_states, boost_state, beta, blank, k,
+             mode, want_rows=True):
+    """One decode step with several LMs (Eq. (1): one weighted term per LM, added
+    in the given order).  ``lm_states`` is [n_lm, H]; ``next_lm`` comes back as
+    [n_lm, H, k]."""
+    hs, al, n = _lm_list(lms, alphas)
+    x = np.ascontiguousarray(logits, dtype=np.float32)
+    H, V = x.shape
+    ls = np.ascontiguousarray(np.asarray(lm_states).reshape(n, H), dtype=np.int32)
+    bs = np.ascontiguousarray(boost_state, dtype=np.int32)
+    key = np.empty((H, V), np.float32) if want_rows else None
+    fused = np.empty((H, V), np.float64) if want_rows else None
+    lse = np.empty(H, np.float64)
+    tok = np.empty((H, k), np.int32)
+    sc = np.empty((H, k), np.float64)
+    nl = np.empty((n, H, k), np.int32)
+    nb = np.empty((H, k), np.int32)
+    rc = lib().or_step_lms(hs, _p(al, ctypes.c_float), n, trie.h if trie is not None else None,
+                           _p(x, ctypes.c_float), _p(ls, ctypes.c_int32), _p(bs, ctypes.c_int32), H,
+                           V, float(beta), int(blank), int(k), int(mode), _p(key, ctypes.c_float),
+                           _p(fused, ctypes.c_double), _p(lse, ctypes.c_double),
+                           _p(tok, ctypes.c_int32), _p(sc, ctypes.c_double), _p(nl, ctypes.c_int32),
+                           _p(nb, ctypes.c_int32))
+    if rc != 0:
+        raise OracleError(_err())
+    return dict(key=key, fused=fused, lse=lse, tokens=tok, scores=sc, next_lm=nl, next_boost=nb)
+
+
+def run_lms(lms, alphas, trie: OracleTrie | None, logits, S, B, k, beta, blank, mode, lm_states,
+            boost_state, hyp_score=None, forced_tokens=None, forced_parents=None, tol=1e-4,
+            threads=1):
+    """``run`` with several LMs: ``lm_states`` is [n_lm, S*B] and the final LM
+    states come back as [n_lm, S*B]."""
+    hs_, al, n = _lm_list(lms, alphas)
+    x = np.ascontiguousarray(logits, dtype=np.float32)
+    T, H, V = x.shape
+    assert H == S * B
+    ls = np.ascontiguousarray(np.asarray(lm_states).reshape(n, H), dtype=np.int32)
+    bs = np.ascontiguousarray(boost_state, dtype=np.int32)
+    hs = None
+    if B > 1:
+        hs = np.ascontiguousarray(hyp_score if hyp_score is not None else
+                                  np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S),
+                                  dtype=np.float64)
+    tok = np.empty((T, H), np.int32)
+    par = np.empty((T, H), np.int32) if B > 1 else None
+    sel = np.empty((T, H), np.float64)
+    lo = np.empty((n, H), np.int32)
+    bo = np.empty(H, np.int32)
+    so = np.empty(H, np.float64)
+    ft = None if forced_tokens is None else np.ascontiguousarray(forced_tokens, dtype=np.int32)
+    fp = None if forced_parents is None else np.ascontiguousarray(forced_parents, dtype=np.int32)
+    near = np.zeros(max(S, 1), np.int64)
+    mis = np.zeros(max(S, 1), np.int64)
+    rc = lib().or_run_lms(hs_, _p(al, ctypes.c_float), n, trie.h if trie is not None else None,
+                          _p(x, ctypes.c_float), T, S, B, V, int(k), float(beta), int(blank),
+                          int(mode), _p(ls, ctypes.c_int32), _p(bs, ctypes.c_int32),
+                          _p(hs, ctypes.c_double), _p(tok, ctypes.c_int32), _p(par, ctypes.c_int32),
+                          _p(sel, ctypes.c_double), _p(lo, ctypes.c_int32), _p(bo, ctypes.c_int32),
+                          _p(so, ctypes.c_double), _p(ft, ctypes.c_int32), _p(fp, ctypes.c_int32),
+                          float(tol), _p(near, ctypes.c_int64), _p(mis, ctypes.c_int64),
+                          int(threads))
     if rc != 0:
         raise OracleError(_err())
     return dict(tokens=tok, parents=par, sel_score=sel, lm_state=lo, boost_state=bo,

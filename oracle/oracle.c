@@ -7,8 +7,9 @@
  *
  * What it computes (paper, Sec. III-C, Eq. (1)): for every hypothesis and
  * every vocabulary token y,
- *     score(y) = log p_AM(y|x) + lambda * log p_LM(y) + beta * boost(y)
- * with one backoff n-gram LM (one alpha_i, written lambda) and a phrase boost,
+ *     score(y) = log p_AM(y|x) + sum_i alpha_i * log p_LM,i(y) + beta * boost(y)
+ * with one or more backoff n-gram LMs (each with its own weight alpha_i and
+ * its own state; with one LM the weight is written lambda) and a phrase boost,
  * followed by greedy (Sec. III, the decoder emits text greedily) or top-k
  * selection, and the advance of the LM and phrase states.
  *
@@ -27,7 +28,8 @@
  *   mode A (greedy default): the acoustic argmax decides blank vs. emit and the
  *   fused score re-ranks the non-blank tokens; mode B: blank competes with key
  *   x_blank; ties go to the lowest token id; the boost is a potential
- *   difference over phrase prefixes (see score_row below).
+ *   difference over phrase prefixes (see score_row below); the LM terms are
+ *   added in the order the models are given, before the boost term.
  */
 #include <math.h>
 #include <pthread.h>
@@ -37,6 +39,7 @@
 #include <string.h>
 
 #define OR_MAXN 16
+#define OR_MAXLM 4 /* LMs per call */
 #define OR_OK 0
 #define OR_EARG (-1)
 #define OR_ENOMEM (-2)
@@ -491,17 +494,20 @@ int64_t or_trie_state_of_history(const OrTrie *t, const int32_t *h, int len) {
 /* one hypothesis, one frame                                                  */
 /* ------------------------------------------------------------------------ */
 typedef struct {
-  const OrLM *lm;
+  const OrLM *lm[OR_MAXLM];
+  float lam[OR_MAXLM]; /* alpha_i of each LM */
+  int n_lm;
   const OrTrie *tr;
   int V, blank, k, mode;
-  float lam, beta;
+  float beta;
 } Ctx;
 
-/* Histories: the LM context is the last <= N-1 tokens of <s> + emitted
-   tokens; the phrase history is the emitted tokens (or, step-wise, the tuple
-   of the incoming state).  Fills key32[V], f64[V] (fused reference score),
-   next_q[V] (phrase state after y); returns lse in fp64. */
-static double score_row(const Ctx *c, const float *x, const int32_t *lmh, int lmlen,
+/* Histories: the context of LM i is the last <= N_i-1 tokens of its history
+   (<s> or the tuple of its incoming state, then the emitted tokens); the
+   phrase history is the emitted tokens (or, step-wise, the tuple of the
+   incoming state).  Fills key32[V], f64[V] (fused reference score), next_q[V]
+   (phrase state after y); returns lse in fp64. */
+static double score_row(const Ctx *c, const float *x, int32_t *const *lmh, const int *lmlen,
                         const int32_t *ph, int plen, float *key32, double *f64, int64_t *next_q) {
   int V = c->V;
   double m = -INFINITY;
@@ -509,9 +515,13 @@ static double score_row(const Ctx *c, const float *x, const int32_t *lmh, int lm
   double s = 0.0;
   for (int y = 0; y < V; ++y) s += exp((double)x[y] - m);
   double lse = m + log(s);
-  int N1 = c->lm->N - 1;
-  const int32_t *ctx = lmlen > N1 ? lmh + (lmlen - N1) : lmh;
-  int clen = lmlen > N1 ? N1 : lmlen;
+  const int32_t *ctx[OR_MAXLM];
+  int clen[OR_MAXLM];
+  for (int i = 0; i < c->n_lm; ++i) {
+    int N1 = c->lm[i]->N - 1;
+    ctx[i] = lmlen[i] > N1 ? lmh[i] + (lmlen[i] - N1) : lmh[i];
+    clen[i] = lmlen[i] > N1 ? N1 : lmlen[i];
+  }
   /* current phrase state and its potential */
   int64_t q = c->tr ? or_trie_state_of_history(c->tr, ph, plen) : 0;
   float phi_q = c->tr ? c->tr->phi[q] : 0.0f;
@@ -525,8 +535,16 @@ static double score_row(const Ctx *c, const float *x, const int32_t *lmh, int lm
       next_q[y] = q;
       continue;
     }
-    float l32 = or_lm_logp32(c->lm, ctx, clen, y);
-    double l64 = or_lm_logp64(c->lm, ctx, clen, y);
+    /* the LM terms in model order: u = fl(... fl(x + fl(a_1 l_1)) ... + fl(a_n l_n)) */
+    float u = x[y];
+    double acc64 = (double)x[y] - lse;
+    for (int i = 0; i < c->n_lm; ++i) {
+      float l32 = or_lm_logp32(c->lm[i], ctx[i], clen[i], y);
+      double l64 = or_lm_logp64(c->lm[i], ctx[i], clen[i], y);
+      float a = c->lam[i] * l32;
+      u = u + a;
+      acc64 = acc64 + (double)c->lam[i] * l64;
+    }
     float b32 = 0.0f;
     double b64 = 0.0;
     int64_t nq = 0;
@@ -536,11 +554,9 @@ static double score_row(const Ctx *c, const float *x, const int32_t *lmh, int lm
       b32 = c->tr->E[nq] - phi_q;
       b64 = c->tr->E64[nq] - phi_q64;
     }
-    float a = c->lam * l32;
-    float u = x[y] + a;
     float v = c->beta * b32;
     key32[y] = u + v;
-    f64[y] = (double)x[y] - lse + (double)c->lam * l64 + (double)c->beta * b64;
+    f64[y] = acc64 + (double)c->beta * b64;
     next_q[y] = nq;
   }
   free(buf);
@@ -587,30 +603,48 @@ static int select_tokens(const Ctx *c, const float *x, const float *key32, int32
 /* step-wise entry: incoming states given as ids                              */
 /* ------------------------------------------------------------------------ */
 /* For each hypothesis h: selected tokens [H,k] (unused slots -1), reference
-   fused scores [H,k] (fp64), next LM / phrase states [H,k]; optionally
-   key32 [H,V], fused64 [H,V], lse64 [H].  Returns 0 or a negative code. */
-int or_step(const OrLM *lm, const OrTrie *tr, const float *logits, const int32_t *lm_state,
-            const int32_t *boost_state, int H, int V, float lam, float beta, int blank, int k,
-            int mode, float *key_out, double *fused_out, double *lse_out, int32_t *tokens,
-            double *scores, int32_t *next_lm, int32_t *next_boost) {
+   fused scores [H,k] (fp64), next LM states [n_lm][H][k] and next phrase
+   states [H,k]; optionally key32 [H,V], fused64 [H,V], lse64 [H].  lm_state is
+   [n_lm][H].  Returns 0 or a negative code. */
+int or_step_lms(const OrLM *const *lms, const float *lams, int n_lm, const OrTrie *tr,
+                const float *logits, const int32_t *lm_state, const int32_t *boost_state, int H, int V,
+                float beta, int blank, int k, int mode, float *key_out, double *fused_out,
+                double *lse_out, int32_t *tokens, double *scores, int32_t *next_lm,
+                int32_t *next_boost) {
   g_err[0] = 0;
-  if (!lm || V != lm->V || blank != lm->blank || H < 0 || k < 1 || k > V || k > 64 ||
+  if (n_lm < 1 || n_lm > OR_MAXLM || !lms || !lams || H < 0 || k < 1 || k > V || k > 64 ||
       (mode == 0 && k != 1))
     return fail(OR_EARG, "bad step arguments");
-  Ctx c = {lm, tr, V, blank, k, mode, lam, beta};
+  Ctx c;
+  memset(&c, 0, sizeof c);
+  for (int i = 0; i < n_lm; ++i) {
+    if (!lms[i] || V != lms[i]->V || blank != lms[i]->blank) return fail(OR_EARG, "bad step arguments");
+    c.lm[i] = lms[i];
+    c.lam[i] = lams[i];
+  }
+  c.n_lm = n_lm;
+  c.tr = tr;
+  c.V = V;
+  c.blank = blank;
+  c.k = k;
+  c.mode = mode;
+  c.beta = beta;
   float *key = (float *)malloc((size_t)V * sizeof(float));
   double *f64 = (double *)malloc((size_t)V * sizeof(double));
   int64_t *nq = (int64_t *)malloc((size_t)V * sizeof(int64_t));
   int32_t sel[64];
-  int32_t lmt[OR_MAXN + 2];
+  int32_t lmt[OR_MAXLM][OR_MAXN + 2];
+  int32_t *lmp[OR_MAXLM];
+  int lmlen[OR_MAXLM];
+  for (int i = 0; i < OR_MAXLM; ++i) lmp[i] = lmt[i];
   int32_t *pt = (int32_t *)malloc((size_t)(tr ? tr->maxlen + 1 : 1) * sizeof(int32_t));
   int rc = OR_OK;
   for (int h = 0; h < H && rc == OR_OK; ++h) {
-    int lmlen = or_lm_state_tuple(lm, lm_state[h], lmt);
-    if (lmlen < 0 || (lmlen == 1 && lmt[0] == blank)) {
-      rc = fail(OR_EARG, "invalid LM state");
-      break;
+    for (int i = 0; i < n_lm; ++i) {
+      lmlen[i] = or_lm_state_tuple(lms[i], lm_state[(int64_t)i * H + h], lmt[i]);
+      if (lmlen[i] < 0 || (lmlen[i] == 1 && lmt[i][0] == blank)) rc = fail(OR_EARG, "invalid LM state");
     }
+    if (rc != OR_OK) break;
     int plen = 0;
     if (tr) {
       plen = or_trie_node_tuple(tr, boost_state[h], pt);
@@ -620,32 +654,27 @@ int or_step(const OrLM *lm, const OrTrie *tr, const float *logits, const int32_t
       }
     }
     const float *x = logits + (int64_t)h * V;
-    double lse = score_row(&c, x, lmt, lmlen, pt, plen, key, f64, nq);
+    double lse = score_row(&c, x, lmp, lmlen, pt, plen, key, f64, nq);
     if (key_out) memcpy(key_out + (int64_t)h * V, key, (size_t)V * sizeof(float));
     if (fused_out) memcpy(fused_out + (int64_t)h * V, f64, (size_t)V * sizeof(double));
     if (lse_out) lse_out[h] = lse;
     int ns = select_tokens(&c, x, key, sel);
     for (int j = 0; j < k; ++j) {
       int64_t o = (int64_t)h * k + j;
-      if (j >= ns) {
-        tokens[o] = -1;
-        scores[o] = -INFINITY;
-        next_lm[o] = lm_state[h];
-        next_boost[o] = boost_state[h];
-        continue;
-      }
-      int y = sel[j];
+      int y = j < ns ? sel[j] : -1;
       tokens[o] = y;
-      scores[o] = f64[y];
-      if (y == blank) {
-        next_lm[o] = lm_state[h];
-        next_boost[o] = boost_state[h];
-      } else {
-        int32_t hist[OR_MAXN + 2];
-        memcpy(hist, lmt, (size_t)lmlen * sizeof(int32_t));
-        hist[lmlen] = y;
-        next_lm[o] = (int32_t)or_lm_state_of_history(lm, hist, lmlen + 1);
-        next_boost[o] = (int32_t)nq[y];
+      scores[o] = j < ns ? f64[y] : -INFINITY;
+      next_boost[o] = (y < 0 || y == blank) ? boost_state[h] : (int32_t)nq[y];
+      for (int i = 0; i < n_lm; ++i) {
+        int64_t oi = (int64_t)i * H * k + o;
+        if (y < 0 || y == blank) {
+          next_lm[oi] = lm_state[(int64_t)i * H + h];
+        } else {
+          int32_t hist[OR_MAXN + 2];
+          memcpy(hist, lmt[i], (size_t)lmlen[i] * sizeof(int32_t));
+          hist[lmlen[i]] = y;
+          next_lm[oi] = (int32_t)or_lm_state_of_history(lms[i], hist, lmlen[i] + 1);
+        }
       }
     }
   }
@@ -656,12 +685,21 @@ int or_step(const OrLM *lm, const OrTrie *tr, const float *logits, const int32_t
   return rc;
 }
 
+/* one LM: or_step_lms with n_lm = 1 and alpha_1 = lam */
+int or_step(const OrLM *lm, const OrTrie *tr, const float *logits, const int32_t *lm_state,
+            const int32_t *boost_state, int H, int V, float lam, float beta, int blank, int k,
+            int mode, float *key_out, double *fused_out, double *lse_out, int32_t *tokens,
+            double *scores, int32_t *next_lm, int32_t *next_boost) {
+  return or_step_lms(&lm, &lam, 1, tr, logits, lm_state, boost_state, H, V, beta, blank, k, mode,
+                     key_out, fused_out, lse_out, tokens, scores, next_lm, next_boost);
+}
+
 /* ------------------------------------------------------------------------ */
 /* free-running decode over T frames from full histories                      */
 /* ------------------------------------------------------------------------ */
 typedef struct {
-  int32_t *lm_hist; /* <s>-prefixed LM history (initial state tuple + emitted) */
-  int lm_len;
+  int32_t *lm_hist[OR_MAXLM]; /* per LM: its initial state tuple + emitted tokens */
+  int lm_len[OR_MAXLM];
   int32_t *ph_hist; /* phrase history (initial node tuple + emitted) */
   int ph_len;
   double score;
@@ -671,11 +709,11 @@ typedef struct {
   const Ctx *c;
   const float *logits;
   int T, S, B, V;
-  const int32_t *lm0, *q0;
+  const int32_t *lm0, *q0; /* lm0: [n_lm][H] */
   const double *score0;
   int32_t *tokens, *parents; /* [T,H] */
   double *sel_score;         /* [T,H]: fused64 of the pick (B == 1) or the new score (B > 1) */
-  int32_t *lm_out, *q_out;
+  int32_t *lm_out, *q_out; /* lm_out: [n_lm][H] */
   double *score_out;
   const int32_t *forced_tok, *forced_par; /* teacher forcing [T,H] or NULL */
   double tol;
@@ -684,9 +722,18 @@ typedef struct {
   int rc;
 } RunJob;
 
-static void hyp_push(Hyp *h, int32_t y) {
-  h->lm_hist[h->lm_len++] = y;
+static void hyp_push(Hyp *h, int n_lm, int32_t y) {
+  for (int i = 0; i < n_lm; ++i) h->lm_hist[i][h->lm_len[i]++] = y;
   h->ph_hist[h->ph_len++] = y;
+}
+
+static void hyp_copy(Hyp *d, const Hyp *p, int n_lm) {
+  for (int i = 0; i < n_lm; ++i) {
+    memcpy(d->lm_hist[i], p->lm_hist[i], (size_t)p->lm_len[i] * sizeof(int32_t));
+    d->lm_len[i] = p->lm_len[i];
+  }
+  memcpy(d->ph_hist, p->ph_hist, (size_t)p->ph_len * sizeof(int32_t));
+  d->ph_len = p->ph_len;
 }
 
 /* candidate of a beam step */
@@ -717,18 +764,24 @@ static void *run_streams(void *arg) {
   int32_t *csel = (int32_t *)malloc((size_t)B * k * sizeof(int32_t));
   double *cf = (double *)malloc((size_t)B * k * sizeof(double));
   for (int b = 0; b < B; ++b) {
-    hy[b].lm_hist = (int32_t *)malloc((size_t)cap * sizeof(int32_t));
+    for (int i = 0; i < c->n_lm; ++i) {
+      hy[b].lm_hist[i] = (int32_t *)malloc((size_t)cap * sizeof(int32_t));
+      nh[b].lm_hist[i] = (int32_t *)malloc((size_t)cap * sizeof(int32_t));
+    }
     hy[b].ph_hist = (int32_t *)malloc((size_t)cap * sizeof(int32_t));
-    nh[b].lm_hist = (int32_t *)malloc((size_t)cap * sizeof(int32_t));
     nh[b].ph_hist = (int32_t *)malloc((size_t)cap * sizeof(int32_t));
   }
   for (int s = J->s_begin; s < J->s_end && J->rc == OR_OK; ++s) {
     for (int b = 0; b < B; ++b) {
       int h = s * B + b;
       Hyp *p = &hy[b];
-      p->lm_len = or_lm_state_tuple(c->lm, J->lm0[h], p->lm_hist);
+      int bad = 0;
+      for (int i = 0; i < c->n_lm; ++i) {
+        p->lm_len[i] = or_lm_state_tuple(c->lm[i], J->lm0[(int64_t)i * H + h], p->lm_hist[i]);
+        bad |= p->lm_len[i] < 0;
+      }
       p->ph_len = c->tr ? or_trie_node_tuple(c->tr, J->q0[h], p->ph_hist) : 0;
-      if (p->lm_len < 0 || p->ph_len < 0) {
+      if (bad || p->ph_len < 0) {
         J->rc = OR_EARG;
         break;
       }
@@ -762,7 +815,7 @@ static void *run_streams(void *arg) {
         }
         J->tokens[(int64_t)t * H + h] = y;
         if (J->sel_score) J->sel_score[(int64_t)t * H + h] = cand[0].score;
-        if (y != c->blank) hyp_push(&hy[0], y);
+        if (y != c->blank) hyp_push(&hy[0], c->n_lm, y);
         continue;
       }
       /* beam: order candidates (score desc, parent asc, rank asc), keep B */
@@ -831,21 +884,13 @@ static void *run_streams(void *arg) {
         int64_t o = (int64_t)t * H + s * B + i;
         Hyp *d = &nh[i];
         if (i < keep) {
-          const Hyp *p = &hy[pick[i].b];
-          memcpy(d->lm_hist, p->lm_hist, (size_t)p->lm_len * sizeof(int32_t));
-          memcpy(d->ph_hist, p->ph_hist, (size_t)p->ph_len * sizeof(int32_t));
-          d->lm_len = p->lm_len;
-          d->ph_len = p->ph_len;
+          hyp_copy(d, &hy[pick[i].b], c->n_lm);
           d->score = pick[i].score;
-          if (pick[i].y != c->blank) hyp_push(d, pick[i].y);
+          if (pick[i].y != c->blank) hyp_push(d, c->n_lm, pick[i].y);
           J->tokens[o] = pick[i].y;
           J->parents[o] = pick[i].b;
         } else {
-          const Hyp *p = &hy[i]; /* empty slot keeps its own history */
-          memcpy(d->lm_hist, p->lm_hist, (size_t)p->lm_len * sizeof(int32_t));
-          memcpy(d->ph_hist, p->ph_hist, (size_t)p->ph_len * sizeof(int32_t));
-          d->lm_len = p->lm_len;
-          d->ph_len = p->ph_len;
+          hyp_copy(d, &hy[i], c->n_lm); /* empty slot keeps its own history */
           d->score = -INFINITY;
           J->tokens[o] = -1;
           J->parents[o] = -1;
@@ -861,15 +906,18 @@ static void *run_streams(void *arg) {
     for (int b = 0; b < B; ++b) {
       int h = s * B + b;
       Hyp *p = &hy[b];
-      J->lm_out[h] = (int32_t)or_lm_state_of_history(c->lm, p->lm_hist, p->lm_len);
+      for (int i = 0; i < c->n_lm; ++i)
+        J->lm_out[(int64_t)i * H + h] = (int32_t)or_lm_state_of_history(c->lm[i], p->lm_hist[i], p->lm_len[i]);
       J->q_out[h] = c->tr ? (int32_t)or_trie_state_of_history(c->tr, p->ph_hist, p->ph_len) : 0;
       if (J->score_out) J->score_out[h] = p->score;
     }
   }
   for (int b = 0; b < B; ++b) {
-    free(hy[b].lm_hist);
+    for (int i = 0; i < c->n_lm; ++i) {
+      free(hy[b].lm_hist[i]);
+      free(nh[b].lm_hist[i]);
+    }
     free(hy[b].ph_hist);
-    free(nh[b].lm_hist);
     free(nh[b].ph_hist);
   }
   free(hy);
@@ -891,18 +939,32 @@ static void *run_streams(void *arg) {
    forced pick that is not within tol of the oracle's own choice is recorded
    in mismatch_at[s] (first frame, else -1); accepted near ties are counted.
    Threads split the streams. */
-int or_run(const OrLM *lm, const OrTrie *tr, const float *logits, int T, int S, int B, int V,
-           int k, float lam, float beta, int blank, int mode, const int32_t *lm_state,
-           const int32_t *boost_state, const double *hyp_score, int32_t *tokens, int32_t *parents,
-           double *sel_score, int32_t *lm_out, int32_t *boost_out, double *score_out,
-           const int32_t *forced_tok, const int32_t *forced_par, double tol, int64_t *near_ties,
-           int64_t *mismatch_at, int n_threads) {
+int or_run_lms(const OrLM *const *lms, const float *lams, int n_lm, const OrTrie *tr,
+               const float *logits, int T, int S, int B, int V, int k, float beta, int blank,
+               int mode, const int32_t *lm_state, const int32_t *boost_state,
+               const double *hyp_score, int32_t *tokens, int32_t *parents, double *sel_score,
+               int32_t *lm_out, int32_t *boost_out, double *score_out, const int32_t *forced_tok,
+               const int32_t *forced_par, double tol, int64_t *near_ties, int64_t *mismatch_at,
+               int n_threads) {
   g_err[0] = 0;
-  if (!lm || V != lm->V || blank != lm->blank || T < 0 || S < 0 || B < 1 || B > 64 || k < 1 ||
+  if (n_lm < 1 || n_lm > OR_MAXLM || !lms || !lams || T < 0 || S < 0 || B < 1 || B > 64 || k < 1 ||
       k > V || (B == 1 && k != 1) || (mode == 0 && k != 1) || (B > 1 && (!parents || !hyp_score)))
     return fail(OR_EARG, "bad run arguments");
   if (B * k > 4096) return fail(OR_EARG, "too many candidates");
-  Ctx c = {lm, tr, V, blank, k, mode, lam, beta};
+  Ctx c;
+  memset(&c, 0, sizeof c);
+  for (int i = 0; i < n_lm; ++i) {
+    if (!lms[i] || V != lms[i]->V || blank != lms[i]->blank) return fail(OR_EARG, "bad run arguments");
+    c.lm[i] = lms[i];
+    c.lam[i] = lams[i];
+  }
+  c.n_lm = n_lm;
+  c.tr = tr;
+  c.V = V;
+  c.blank = blank;
+  c.k = k;
+  c.mode = mode;
+  c.beta = beta;
   if (n_threads < 1) n_threads = 1;
   if (n_threads > S) n_threads = S > 0 ? S : 1;
   for (int s = 0; s < S; ++s) {
@@ -953,4 +1015,16 @@ int or_run(const OrLM *lm, const OrTrie *tr, const float *logits, int T, int S, 
   free(jobs);
   free(th);
   return rc;
+}
+
+/* one LM: or_run_lms with n_lm = 1 and alpha_1 = lam */
+int or_run(const OrLM *lm, const OrTrie *tr, const float *logits, int T, int S, int B, int V,
+           int k, float lam, float beta, int blank, int mode, const int32_t *lm_state,
+           const int32_t *boost_state, const double *hyp_score, int32_t *tokens, int32_t *parents,
+           double *sel_score, int32_t *lm_out, int32_t *boost_out, double *score_out,
+           const int32_t *forced_tok, const int32_t *forced_par, double tol, int64_t *near_ties,
+           int64_t *mismatch_at, int n_threads) {
+  return or_run_lms(&lm, &lam, 1, tr, logits, T, S, B, V, k, beta, blank, mode, lm_state,
+                    boost_state, hyp_score, tokens, parents, sel_score, lm_out, boost_out, score_out,
+                    forced_tok, forced_par, tol, near_ties, mismatch_at, n_threads);
 }

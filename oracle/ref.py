@@ -1,8 +1,8 @@
 """Pure-Python statement of the fusion step for tiny inputs (test infrastructure).
 
 A second, independent implementation of the same definitions as ``oracle.c``
-(Eq. (1) of the paper with one LM, ARPA backoff, phrase prefixes by direct
-suffix comparison), used to cross-check the C oracle on small random cases.
+(Eq. (1) of the paper with one or several LMs, ARPA backoff, phrase prefixes
+by direct suffix comparison), used to cross-check the C oracle on small random cases.
 Dictionaries and tuples only; fp32 steps use numpy float32 scalars so every
 operation rounds once.
 """
@@ -138,6 +138,33 @@ def score_row(lm: RefLM, trie: RefTrie | None, x, lm_hist, ph_hist, lam, beta, b
         b64 = trie.boost(ph_hist, y, wide=True) if trie is not None else 0.0
         key[y] = f32(f32(xv + f32(lam * l32)) + f32(beta * b32))
         fused[y] = float(xv) - lse + float(lam) * l64 + float(beta) * b64
+    return key, fused, lse
+
+
+def score_row_lms(lms, lams, trie: RefTrie | None, x, lm_hists, ph_hist, beta, blank):
+    """score_row with several LMs, each with its own history and weight; the LM
+    terms are added in the given order, then the boost term."""
+    V = len(x)
+    m = max(float(v) for v in x)
+    lse = m + math.log(sum(math.exp(float(v) - m) for v in x))
+    lams, beta = [f32(a) for a in lams], f32(beta)
+    key = np.empty(V, np.float32)
+    fused = np.empty(V, np.float64)
+    for y in range(V):
+        xv = f32(x[y])
+        if y == blank:
+            key[y] = xv
+            fused[y] = float(xv) - lse
+            continue
+        u = xv
+        acc = float(xv) - lse
+        for lm, lam, hist in zip(lms, lams, lm_hists):
+            u = f32(u + f32(lam * lm.logp(hist, y)))
+            acc = acc + float(lam) * lm.logp(hist, y, wide=True)
+        b32 = trie.boost(ph_hist, y) if trie is not None else f32(0.0)
+        b64 = trie.boost(ph_hist, y, wide=True) if trie is not None else 0.0
+        key[y] = f32(u + f32(beta * b32))
+        fused[y] = acc + float(beta) * b64
     return key, fused, lse
 
 
