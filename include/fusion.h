@@ -81,6 +81,7 @@ enum { FUSION_STATUS_BAD_LM_STATE = 1, FUSION_STATUS_BAD_BOOST_STATE = 2,
 #define FUSION_MAX_VOCAB 8190
 #define FUSION_MAX_K 8
 #define FUSION_MAX_BEAM 32
+#define FUSION_MAX_LMS 2     /* LMs per fusion_step_lms / fusion_run_lms call (2 needs V <= 4096) */
 
 typedef struct NgramTables NgramTables; /* opaque, device resident, immutable after load */
 typedef struct BoostTrie BoostTrie;     /* opaque, device resident, immutable after build */
@@ -186,6 +187,32 @@ int fusion_run(const NgramTables *lm, const BoostTrie *trie, const float *logits
                int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state,
                double *hyp_score, int32_t *tokens, int32_t *parents, float *fused,
                int64_t *traffic, hipStream_t stream);
+
+/*
+ * fusion_step_lms / fusion_run_lms - fusion_step / fusion_run with several
+ * n-gram LMs, the sum over i of alpha_i * log p_LM,i(y) in Eq. (1) (Sec. III-C):
+ * each LM has its own weight and its own state, advanced by the same tokens.
+ *   lms, alphas  host arrays of n_lm handles and weights, 1 <= n_lm <= FUSION_MAX_LMS;
+ *                every LM must have the call's vocab and blank_id (orders may differ)
+ *   lm_state     device [n_lm, H] state ids (LM i's state of hypothesis h at
+ *                i * H + h); fusion_run_lms writes the final states back there
+ *   next_lm      (step) device [n_lm, H, k]: LM i's state after each selection
+ * Every other argument is as in fusion_step / fusion_run (beta is the boost
+ * weight).  Keys are fp32 with one rounding per operation, the LM terms added
+ * in the order of lms: key = (...((x + a_1 lm_1) + a_2 lm_2)...) + beta boost.
+ * With n_lm == 1 the calls are fusion_step / fusion_run with lambda = alphas[0].
+ * Two LMs with V > 4096 return FUSION_E_UNSUPPORTED (LDS).
+ */
+int fusion_step_lms(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
+                    const BoostTrie *trie, const float *logits, const int32_t *lm_state,
+                    const int32_t *boost_state, int32_t H, int32_t V, float beta, int32_t blank_id,
+                    int32_t k, int32_t blank_mode, float *fused, int32_t *tokens, float *scores,
+                    int32_t *next_lm, int32_t *next_boost, hipStream_t stream);
+int fusion_run_lms(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
+                   const BoostTrie *trie, const float *logits, int32_t T, int32_t S, int32_t B,
+                   int32_t V, int32_t k, float beta, int32_t blank_id, int32_t blank_mode,
+                   int32_t *lm_state, int32_t *boost_state, double *hyp_score, int32_t *tokens,
+                   int32_t *parents, float *fused, int64_t *traffic, hipStream_t stream);
 
 /*
  * joint_project - output projection of the Transducer joint network (the

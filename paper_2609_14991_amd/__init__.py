@@ -30,9 +30,11 @@ FUSION_BLANK_COMPETE = 1
 FUSION_STATUS_BAD_LM_STATE = 1
 FUSION_STATUS_BAD_BOOST_STATE = 2
 
+FUSION_MAX_LMS = 2
+
 EXPORTS = ("ngram_load", "ngram_bos_state", "ngram_info", "ngram_free", "boost_build", "boost_info",
-           "boost_free", "fusion_step", "fusion_run", "joint_project", "fusion_last_error",
-           "fusion_device_status")
+           "boost_free", "fusion_step", "fusion_run", "fusion_step_lms", "fusion_run_lms",
+           "joint_project", "fusion_last_error", "fusion_device_status")
 
 
 class FusionError(RuntimeError):
@@ -74,6 +76,12 @@ def lib():
         L.fusion_run.restype = ctypes.c_int
         L.fusion_run.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, f32, f32, i32, i32, vp, vp, vp,
                                  vp, vp, vp, vp, vp]
+        L.fusion_step_lms.restype = ctypes.c_int
+        L.fusion_step_lms.argtypes = [vp, vp, i32, vp, vp, vp, vp, i32, i32, f32, i32, i32, i32, vp,
+                                      vp, vp, vp, vp, vp]
+        L.fusion_run_lms.restype = ctypes.c_int
+        L.fusion_run_lms.argtypes = [vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f32, i32, i32, vp,
+                                     vp, vp, vp, vp, vp, vp, vp]
         L.joint_project.restype = ctypes.c_int
         L.joint_project.argtypes = [vp, vp, vp, i32, i32, i32, vp, vp]
         L.fusion_last_error.restype = ctypes.c_char_p
@@ -223,6 +231,39 @@ def fusion_run(lm, trie, logits, T, S, B, V, k, lam, beta, blank_id, blank_mode,
                             _ptr(fused), _ptr(traffic), _stream(stream)))
 
 
+def _lm_arrays(lms, alphas):
+    """Host arrays of handles and weights for the several-LM calls."""
+    lms, alphas = list(lms), [float(a) for a in alphas]
+    if len(lms) != len(alphas):
+        raise ValueError("one weight per LM")
+    hs = (ctypes.c_void_p * max(1, len(lms)))(*[m.h.value for m in lms])
+    al = np.array(alphas if alphas else [0.0], dtype=np.float32)
+    return hs, al, len(lms)
+
+
+def fusion_step_lms(lms, alphas, trie, logits, lm_state, boost_state, H, V, beta, blank_id, k,
+                    blank_mode, fused, tokens, scores, next_lm, next_boost, stream=None):
+    """Same arguments as the C call; lms and alphas are Python sequences,
+    tensors are CUDA (HIP) tensors (lm_state [n_lm, H], next_lm [n_lm, H, k])."""
+    hs, al, n = _lm_arrays(lms, alphas)
+    _check(lib().fusion_step_lms(ctypes.cast(hs, ctypes.c_void_p), _ptr(al), n, _h(trie), _ptr(logits),
+                                 _ptr(lm_state), _ptr(boost_state), int(H), int(V), float(beta),
+                                 int(blank_id), int(k), int(blank_mode), _ptr(fused), _ptr(tokens),
+                                 _ptr(scores), _ptr(next_lm), _ptr(next_boost), _stream(stream)))
+
+
+def fusion_run_lms(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
+                   boost_state, hyp_score, tokens, parents, fused=None, traffic=None, stream=None):
+    """Same arguments as the C call; lms and alphas are Python sequences,
+    tensors are CUDA (HIP) tensors (lm_state [n_lm, S*B])."""
+    hs, al, n = _lm_arrays(lms, alphas)
+    _check(lib().fusion_run_lms(ctypes.cast(hs, ctypes.c_void_p), _ptr(al), n, _h(trie), _ptr(logits),
+                                int(T), int(S), int(B), int(V), int(k), float(beta), int(blank_id),
+                                int(blank_mode), _ptr(lm_state), _ptr(boost_state), _ptr(hyp_score),
+                                _ptr(tokens), _ptr(parents), _ptr(fused), _ptr(traffic),
+                                _stream(stream)))
+
+
 def joint_project(A, W, bias, M, N, K, out, stream=None):
     """Same arguments as the C call; A and W are int16/uint16 (bf16 bit patterns) or
     bfloat16 CUDA tensors, bias and out float32 CUDA tensors."""
@@ -281,4 +322,40 @@ def run(lm, trie, logits, S, B, k, lam, beta, blank_id, blank_mode, lm_state, bo
     fused = torch.zeros((T, H, V), dtype=torch.float32, device=dev) if want_fused else None
     fusion_run(lm, trie, logits, T, S, B, V, k, lam, beta, blank_id, blank_mode, lm_state,
                boost_state, hyp_score, tokens, parents, fused, traffic, stream)
+    return dict(tokens=tokens, parents=parents, fused=fused)
+
+
+def step_lms(lms, alphas, trie, logits, lm_state, boost_state, beta, blank_id, k, blank_mode,
+             want_fused=False, stream=None):
+    """``step`` with several LMs: lm_state [n_lm, H]; next_lm comes back [n_lm, H, k]."""
+    import torch
+
+    H, V = logits.shape
+    dev = logits.device
+    n = len(lms)
+    out = dict(
+        tokens=torch.empty((H, k), dtype=torch.int32, device=dev),
+        scores=torch.empty((H, k), dtype=torch.float32, device=dev),
+        next_lm=torch.empty((n, H, k), dtype=torch.int32, device=dev),
+        next_boost=torch.empty((H, k), dtype=torch.int32, device=dev),
+        fused=torch.empty((H, V), dtype=torch.float32, device=dev) if want_fused else None,
+    )
+    fusion_step_lms(lms, alphas, trie, logits, lm_state, boost_state, H, V, beta, blank_id, k,
+                    blank_mode, out["fused"], out["tokens"], out["scores"], out["next_lm"],
+                    out["next_boost"], stream)
+    return out
+
+
+def run_lms(lms, alphas, trie, logits, S, B, k, beta, blank_id, blank_mode, lm_state, boost_state,
+            hyp_score=None, want_fused=False, traffic=None, stream=None):
+    """``run`` with several LMs: lm_state [n_lm, S*B] is updated in place."""
+    import torch
+
+    T, H, V = logits.shape
+    dev = logits.device
+    tokens = torch.empty((T, H), dtype=torch.int32, device=dev)
+    parents = torch.empty((T, H), dtype=torch.int32, device=dev) if B > 1 else None
+    fused = torch.zeros((T, H, V), dtype=torch.float32, device=dev) if want_fused else None
+    fusion_run_lms(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
+                   boost_state, hyp_score, tokens, parents, fused, traffic, stream)
     return dict(tokens=tokens, parents=parents, fused=fused)

@@ -56,13 +56,14 @@ constexpr int kMaxWaves = 16;
 constexpr int kMaxLevels = FUSION_MAX_ORDER;  // context levels 1..N-1 <= 7
 constexpr int kAux = 256;                     // LDS side tables: phrase transitions, top-level next states
 constexpr int kNodeLane = 32;                 // lanes 32..35 of the record word hold the phrase node
+constexpr int kLM1Lane = 40;                  // lanes 40..59 hold the second LM's record
 constexpr int kSpinLimit = 1 << 20;           // bounded wait at the beam rendezvous (polls, ~1 s)
 
 __device__ int g_status;
 __device__ int32_t g_zero_words[4];  // never written: read by lanes that have no record word
 
 struct Params {
-  LMDevice lm;
+  LMDevice lm[FUSION_MAX_LMS];  // the n_lm models of Eq. (1), each with its own weight lam[i]
   TrieDevice tr;
   const float *logits;
   int32_t *lm_state;
@@ -76,8 +77,8 @@ struct Params {
   int32_t *next_lm;
   int32_t *next_boost;
   unsigned long long *xchg;  // beam exchange [S][2][B][k] candidate records of four tagged words
-  int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, pad;
-  float lam, beta;
+  int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, n_lm;
+  float lam[FUSION_MAX_LMS], beta;
 };
 
 __device__ __forceinline__ bool before(float ka, int ya, float kb, int yb) {
@@ -198,50 +199,59 @@ __device__ __forceinline__ void row_best(float &k, int &y) {
 __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // hypothesis state carried between frames (LDS, written by one lane)
+template <int NL>
 struct HypState {
-  int lmsrc, qsrc, y, c1p;  // where the state comes from (see TopK), token, parent's c_1
-  int c1, fl;               // last token of the LM context (-1: from the record); 1 alive, 2 invalid
-  int cur_lm, cur_q;        // ids of the state scored this frame
-  double S;                 // running beam score
+  // per LM: where the next state comes from (an id, or < 0: reached from c1p by
+  // token y), the parent's c_1, the last token of the context (-1: from the
+  // record), the id of the state scored this frame
+  int lmsrc[NL], c1p[NL], c1[NL], cur_lm[NL];
+  int qsrc, y, fl;  // phrase source, token; flags 1 alive, 2 invalid
+  int cur_q;        // phrase state scored this frame
+  double S;         // running beam score
 };
+
+// first lane of LM i's record in the record word
+__device__ __forceinline__ constexpr int rec_lane0(int i) { return i == 0 ? 0 : kLM1Lane; }
 
 // MODE: what a launch computes (the code of the other modes is compiled out)
 constexpr int kModeStep = 0, kModeGreedy = 1, kModeBeam = 2;
 
-template <int W, int NC, int KM, bool AL, int MODE>
+template <int W, int NC, int KM, bool AL, int MODE, int NL>
 __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   constexpr int NW = W / 64;
   constexpr int Vp = NC * 4 * W;
   constexpr int kUA = W >= 1024 ? 1 : 4;  // arcs per lane fetched in the second hop
   constexpr int kUD = W >= 1024 ? 1 : 2;  // phrase transitions per lane fetched in the second hop
   extern __shared__ __align__(16) unsigned char dyn[];
-  // LDS rows, one entry per token: the dense level-1 LM row; the winning explicit
-  // arc (stamp << 48 | level << 45 | offset << 32 | value bits, kept by an atomic
-  // max, so the highest level wins whatever the order of the writes); the phrase
-  // transition overriding the root's (stamp << 16 | transition + 1).  The stamp
-  // is the frame's (t mod 2^15) + 1: entries of earlier frames compare lower and
-  // read as absent, so no per-frame clearing is needed
-  float *lmval = reinterpret_cast<float *>(dyn);
-  unsigned long long *arcw = reinterpret_cast<unsigned long long *>(dyn + 4 * Vp);
-  uint32_t *ptag = reinterpret_cast<uint32_t *>(dyn + 12 * Vp);
-  float *sE = reinterpret_cast<float *>(dyn + 16 * Vp);  // sE[j + 1]: entry value of transition j
+  // LDS rows, one entry per token: per LM, the dense level-1 row and the winning
+  // explicit arc (stamp << 48 | level << 45 | offset << 32 | value bits, kept by
+  // an atomic max, so the highest level wins whatever the order of the writes);
+  // the phrase transition overriding the root's (stamp << 16 | transition + 1).
+  // The stamp is the frame's (t mod 2^15) + 1: entries of earlier frames compare
+  // lower and read as absent, so no per-frame clearing is needed
+  float *lmval = reinterpret_cast<float *>(dyn);                                             // [NL][Vp]
+  unsigned long long *arcw = reinterpret_cast<unsigned long long *>(dyn + 4 * NL * Vp);      // [NL][Vp]
+  uint32_t *ptag = reinterpret_cast<uint32_t *>(dyn + 12 * NL * Vp);
+  float *sE = reinterpret_cast<float *>(dyn + (12 * NL + 4) * Vp);  // sE[j + 1]: entry value of transition j
   int *sDT = reinterpret_cast<int *>(sE + kAux + 4);
-  int *sTN = sDT + kAux;
+  int *sTN = sDT + kAux;  // [NL][kAux]
   __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves];
   __shared__ int s_paid[kMaxWaves];
   __shared__ int w_key[kMaxWaves][KM];  // order-preserving images of the keys (ord_key)
   __shared__ int w_y[kMaxWaves][KM];
-  __shared__ HypState hs;
-  // beam rendezvous staging (wave 0): candidate records, parent flags, totals
+  __shared__ HypState<NL> hs;
+  // beam rendezvous staging (wave 0): candidate records (the second LM's source
+  // and c_1 in s_xb), parent flags, totals
   __shared__ int4 s_xa[FUSION_MAX_BEAM * FUSION_MAX_K];
+  __shared__ int2 s_xb[NL > 1 ? FUSION_MAX_BEAM * FUSION_MAX_K : 1];
   __shared__ int s_xf[FUSION_MAX_BEAM * FUSION_MAX_K];
   __shared__ double s_tot[FUSION_MAX_BEAM * FUSION_MAX_K];
-  __shared__ long long s_sbase[kMaxLevels];  // state id of arc index i of level L < N-1: s_sbase[L] + i
-  __shared__ int s_lbeg[kMaxLevels];  // first arc of each level of the current state
+  __shared__ long long s_sbase[NL][kMaxLevels];  // state id of arc index i of level L < N-1: s_sbase[L] + i
+  __shared__ int s_lbeg[NL][kMaxLevels];  // first arc of each level of the current state
   __shared__ int s_cfg[2];  // V, blank: re-read each frame so per-token masks stay inside the loop
   __shared__ unsigned long long s_bytes, s_steps;
 
-  const LMDevice &lm = p.lm;
+  const LMDevice *lms = p.lm;
   const TrieDevice &tr = p.tr;
   const int g = threadIdx.x;
   // this lane's entries of the arc and phrase rows back to 0 (absent)
@@ -249,16 +259,23 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int y0 = (c * W + g) * 4;
-      *reinterpret_cast<uint4 *>(arcw + y0) = make_uint4(0u, 0u, 0u, 0u);
-      *reinterpret_cast<uint4 *>(arcw + y0 + 2) = make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+      for (int i = 0; i < NL; ++i) {
+        *reinterpret_cast<uint4 *>(arcw + i * Vp + y0) = make_uint4(0u, 0u, 0u, 0u);
+        *reinterpret_cast<uint4 *>(arcw + i * Vp + y0 + 2) = make_uint4(0u, 0u, 0u, 0u);
+      }
       *reinterpret_cast<uint4 *>(ptag + y0) = make_uint4(0u, 0u, 0u, 0u);
     }
   };
   const int wave = g >> 6;
   const int lane = g & 63;
   const int B = MODE == kModeBeam ? p.B : 1, K = p.k;
-  const int N = lm.N;
-  const int RS = lm.rec_stride;
+  int Nl[NL], RSl[NL];  // order and record stride of each LM
+#pragma unroll
+  for (int i = 0; i < NL; ++i) {
+    Nl[i] = lms[i].N;
+    RSl[i] = lms[i].rec_stride;
+  }
   // workgroup -> (stream, hypothesis); with xcd_map the B workgroups of a stream
   // share blockIdx mod 8, i.e. one XCD and its L2, for the per-frame exchange
   int sl, b;
@@ -279,7 +296,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 
   // ---- prologue ------------------------------------------------------------------
   if (g < kMaxLevels) {
-    s_sbase[g] = (g >= 2 && g + 1 <= N - 1) ? lm.off[g + 1] - lm.arc_base[g] : 0;
+#pragma unroll
+    for (int i = 0; i < NL; ++i)
+      s_sbase[i][g] = (g >= 2 && g + 1 <= Nl[i] - 1) ? lms[i].off[g + 1] - lms[i].arc_base[g] : 0;
   }
   if (g == 0) {
     s_cfg[0] = p.V;
@@ -287,19 +306,24 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     s_bytes = 0;
     s_steps = 0;
     const int V = p.V, blank = p.blank;
-    const int sig = p.lm_state[h];
     const int q = p.has_trie ? p.boost_state[h] : 0;
     const double sc = MODE == kModeBeam ? p.hyp_score[h] : 0.0;
-    const bool ok_lm = sig >= 0 && sig < lm.n_states && sig != blank && (sig != V + 1 || lm.eos_ok);
+    bool ok_lm = true;
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int sig = p.lm_state[(int64_t)i * H + h];  // [n_lm][H]
+      const bool ok_i = sig >= 0 && sig < lms[i].n_states && sig != blank && (sig != V + 1 || lms[i].eos_ok);
+      ok_lm = ok_lm && ok_i;
+      hs.lmsrc[i] = sig;
+      hs.c1p[i] = -1;
+      hs.c1[i] = (ok_i && sig < V + 2) ? sig : -1;
+      hs.cur_lm[i] = sig;
+    }
     const bool ok_q = !p.has_trie || (q >= 0 && q < tr.n_nodes);
     const bool alive = MODE != kModeBeam || sc > -INFINITY;
-    hs.lmsrc = sig;
     hs.qsrc = q;
     hs.y = -1;
-    hs.c1p = -1;
-    hs.c1 = (ok_lm && sig < V + 2) ? sig : -1;
     hs.fl = (alive ? 1 : 0) | ((ok_lm && ok_q) ? 0 : 2);
-    hs.cur_lm = sig;
     hs.cur_q = q;
     hs.S = sc;
     if (alive && !(ok_lm && ok_q))
@@ -388,21 +412,22 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       s_paid[sw] = aid;
     }
   };
-  // the level-1 dense row of context token cc straight into the LDS LM row (this
-  // wave's strips)
-  auto load_dense = [&](int cc, int V) {
-    const float *drow = lm.dense + (int64_t)cc * V;
+  // the level-1 dense row of LM i for context token cc straight into its LDS row
+  // (this wave's strips)
+  auto load_dense = [&](int i, int cc, int V) {
+    const float *drow = lms[i].dense + (int64_t)cc * V;
+    float *row = lmval + i * Vp;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int wbase = c * W + wave * 64;  // first 4-token strip of this wave
       if (AL) {
         const int y0 = (wbase + lane) * 4;
-        __builtin_amdgcn_global_load_lds(drow + (y0 < V ? y0 : 0), (lds_ptr_t)(lmval + wbase * 4), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(drow + (y0 < V ? y0 : 0), (lds_ptr_t)(row + wbase * 4), 16, 0, 0);
       } else {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int y = wbase * 4 + j * 64 + lane;
-          __builtin_amdgcn_global_load_lds(drow + (y < V ? y : 0), (lds_ptr_t)(lmval + wbase * 4 + j * 64), 4, 0, 0);
+          __builtin_amdgcn_global_load_lds(drow + (y < V ? y : 0), (lds_ptr_t)(row + wbase * 4 + j * 64), 4, 0, 0);
         }
       }
     }
@@ -423,13 +448,22 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       clear_rows();
       __syncthreads();
     }
-    const int lmsrc = uni(hs.lmsrc), qsrc = uni(hs.qsrc), yin = uni(hs.y);
-    int c1 = uni(hs.c1);
-    // ---- hop 1: state record, phrase node, dense level-1 row ---------------------
-    const int32_t *rp = nullptr;
-    if (ok) {
-      if (lmsrc < 0) rp = lm.rec_dense + ((int64_t)uni(hs.c1p) * V + yin) * RS;
-      else if (lmsrc >= V + 2) rp = lm.rec + (int64_t)(lmsrc - V - 2) * RS;
+    const int qsrc = uni(hs.qsrc), yin = uni(hs.y);
+    int lmsrc[NL], c1[NL];
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      lmsrc[i] = uni(hs.lmsrc[i]);
+      c1[i] = uni(hs.c1[i]);
+    }
+    // ---- hop 1: state records, phrase node, dense level-1 rows ------------------
+    const int32_t *rp[NL];
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      rp[i] = nullptr;
+      if (ok) {
+        if (lmsrc[i] < 0) rp[i] = lms[i].rec_dense + ((int64_t)uni(hs.c1p[i]) * V + yin) * RSl[i];
+        else if (lmsrc[i] >= V + 2) rp[i] = lms[i].rec + (int64_t)(lmsrc[i] - V - 2) * RSl[i];
+      }
     }
     const int4 *np = nullptr;
     if (ok && p.has_trie) np = qsrc < 0 ? tr.root_node + yin : tr.node + qsrc;
@@ -443,68 +477,84 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j) xv[c][j] = (act && (c * W + g) * 4 + j < V) ? xraw[c][j] : -INFINITY;
-    // lanes 0..RS-1: record words; lanes 32..35: phrase node; every other lane,
-    // and every lane without a record or node, reads a zero word.  One load per
-    // lane, used as loaded, so that decoding the record waits for it alone and not
-    // for the dense row and the logits fetched after it
+    // lanes 0..RS-1: record words of the first LM; lanes 32..35: phrase node;
+    // lanes 40..40+RS-1: record words of the second LM; every other lane, and
+    // every lane without a record or node, reads a zero word.  One load per lane,
+    // used as loaded, so that decoding the records waits for them alone and not
+    // for the dense rows and the logits fetched after them
     int rw;
     {
       const int32_t *src = &g_zero_words[0];
-      if (rp && lane < RS) src = rp + lane;
+      if (rp[0] && lane < RSl[0]) src = rp[0] + lane;
       if (np && lane >= kNodeLane && lane < kNodeLane + 4) src = reinterpret_cast<const int *>(np) + (lane - kNodeLane);
+      if (NL > 1 && rp[NL - 1] && lane >= kLM1Lane && lane < kLM1Lane + RSl[NL - 1])
+        src = rp[NL - 1] + (lane - kLM1Lane);
       rw = *src;
     }
-    // the initial state of a run may need its record to learn c_1
-    if (ok && c1 < 0) c1 = rp ? (rdl(rw, 0) & 0xFFFF) : lmsrc;
-    // level-1 dense row straight into the LDS LM row.  Issued unconditionally
-    // (row 0 stands in when the hypothesis has no keys to compute this frame), so
-    // that the record decode can wait for the record alone
-    load_dense(ok ? c1 : 0, V);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      // the initial state of a run may need its record to learn c_1
+      if (ok && c1[i] < 0) c1[i] = rp[i] ? (rdl(rw, rec_lane0(i)) & 0xFFFF) : lmsrc[i];
+      // level-1 dense row straight into the LM's LDS row.  Issued
+      // unconditionally (row 0 stands in when the hypothesis has no keys to
+      // compute this frame), so that the record decode can wait for the record
+      // alone
+      load_dense(i, ok ? c1[i] : 0, V);
+    }
     if (NW == 1 && t > 0) row_stats(xraw, 0, V);  // a single wave has no idle helper
-    // ---- decode the record ------------------------------------------------------
+    // ---- decode the records ---------------------------------------------------------
     // (words a record does not use, the levels above m among them, read as 0, as do
     // the node lanes without a node)
-    const int m = rp ? (rdl(rw, 0) >> 16) : 1;
-    const int sid = rp ? rdl(rw, 1) : lmsrc;
     const float phiq = as_float(rdl(rw, kNodeLane));
     const int dbeg = rdl(rw, kNodeLane + 1);
     const int dcnt = rdl(rw, kNodeLane + 2);
     const int qid = np ? rdl(rw, kNodeLane + 3) : qsrc;
-    // backoffs, first arcs and arc counts of levels 2..7 as uniform values
-    // (readlane at fixed lanes is valid whatever the active mask); adding the
-    // zero backoffs above m changes no sum (at most the sign of a zero)
-    float bo[kMaxLevels];
-    int lcnt[kMaxLevels], lbeg[kMaxLevels];
-    int total_arcs = 0;
+    // per LM: order m of the state, its id; backoffs, first arcs and arc counts of
+    // levels 2..7 as uniform values (readlane at fixed lanes is valid whatever
+    // the active mask); adding the zero backoffs above m changes no sum (at most
+    // the sign of a zero)
+    int m[NL], sid[NL], total_arcs[NL];
+    float bo[NL][kMaxLevels];
+    int lcnt[NL][kMaxLevels], lbeg[NL][kMaxLevels];
 #pragma unroll
-    for (int L = 2; L < kMaxLevels; ++L) {
-      bo[L] = as_float(rdl(rw, rec_bo_lane(L)));
-      lcnt[L] = rdl(rw, rec_cnt_lane(L));
-      lbeg[L] = rdl(rw, rec_beg_lane(L));
-      total_arcs += lcnt[L];
+    for (int i = 0; i < NL; ++i) {
+      const int l0 = rec_lane0(i);
+      m[i] = rp[i] ? (rdl(rw, l0) >> 16) : 1;
+      sid[i] = rp[i] ? rdl(rw, l0 + 1) : lmsrc[i];
+      total_arcs[i] = 0;
+#pragma unroll
+      for (int L = 2; L < kMaxLevels; ++L) {
+        bo[i][L] = as_float(rdl(rw, l0 + rec_bo_lane(L)));
+        lcnt[i][L] = rdl(rw, l0 + rec_cnt_lane(L));
+        lbeg[i][L] = rdl(rw, l0 + rec_beg_lane(L));
+        total_arcs[i] += lcnt[i][L];
+      }
     }
     // ---- hop 2: first arcs of levels 2..m (flattened) and first phrase transitions --
-    int2 ab[kUA];
-    int at[kUA], tn[kUA];  // at = level << 16 | offset within the level
+    int2 ab[NL][kUA];
+    int at[NL][kUA], tn[NL][kUA];  // at = level << 16 | offset within the level
 #pragma unroll
-    for (int u = 0; u < kUA; ++u) {
-      int f = u * W + g;
-      ab[u] = make_int2(INT_MAX, 0);
-      at[u] = 0;
-      tn[u] = 0;
-      // the level of flattened arc f: subtract the counts of the levels below
-      int L = 2, bL = lbeg[2];
+    for (int i = 0; i < NL; ++i) {
 #pragma unroll
-      for (int L2 = 2; L2 < kMaxLevels - 1; ++L2) {
-        const bool past = (L == L2) && (f >= lcnt[L2]);
-        f = past ? f - lcnt[L2] : f;
-        L = past ? L2 + 1 : L;
-        bL = past ? lbeg[L2 + 1] : bL;
-      }
-      if (u * W + g < total_arcs) {
-        at[u] = (L << 16) | f;
-        ab[u] = lm.arcs[bL + f];
-        if (L == N - 1 && f < kAux) tn[u] = lm.top_next[bL + f - lm.arc_base[N - 1]];
+      for (int u = 0; u < kUA; ++u) {
+        int f = u * W + g;
+        ab[i][u] = make_int2(INT_MAX, 0);
+        at[i][u] = 0;
+        tn[i][u] = 0;
+        // the level of flattened arc f: subtract the counts of the levels below
+        int L = 2, bL = lbeg[i][2];
+#pragma unroll
+        for (int L2 = 2; L2 < kMaxLevels - 1; ++L2) {
+          const bool past = (L == L2) && (f >= lcnt[i][L2]);
+          f = past ? f - lcnt[i][L2] : f;
+          L = past ? L2 + 1 : L;
+          bL = past ? lbeg[i][L2 + 1] : bL;
+        }
+        if (u * W + g < total_arcs[i]) {
+          at[i][u] = (L << 16) | f;
+          ab[i][u] = lms[i].arcs[bL + f];
+          if (L == Nl[i] - 1 && f < kAux) tn[i][u] = lms[i].top_next[bL + f - lms[i].arc_base[Nl[i] - 1]];
+        }
       }
     }
     int4 dd[kUD];
@@ -515,25 +565,28 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       if (j < dcnt) dd[u] = tr.delta[dbeg + j];
     }
     if (ok && g == 0) {
-      hs.cur_lm = sid;
       hs.cur_q = qid;
-      hs.c1 = c1;
 #pragma unroll
-      for (int L = 2; L < kMaxLevels; ++L) s_lbeg[L] = lbeg[L];
+      for (int i = 0; i < NL; ++i) {
+        hs.cur_lm[i] = sid[i];
+        hs.c1[i] = c1[i];
+#pragma unroll
+        for (int L = 2; L < kMaxLevels; ++L) s_lbeg[i][L] = lbeg[i][L];
+      }
     }
     // ---- scatter (no ordering between levels: see arcw) ----------------------------
     // an arc of level L is stored summed with the backoffs of levels L+1.., the
     // addition order of the backoff recursion
-    auto put_arc = [&](int L, int j, int2 a, int tnext) {
+    auto put_arc = [&](int i, int L, int j, int2 a, int tnext) {
       const int y = a.x;
       if (y < V) {
         float v = as_float(a.y);
 #pragma unroll
-        for (int L2 = 3; L2 < kMaxLevels; ++L2) v = v + (L2 > L ? bo[L2] : 0.0f);
+        for (int L2 = 3; L2 < kMaxLevels; ++L2) v = v + (L2 > L ? bo[i][L2] : 0.0f);
         const uint32_t tag = (stamp << 16) | (uint32_t)((L << 13) | j);
-        __hip_atomic_fetch_max(arcw + y, ((unsigned long long)tag << 32) | (unsigned long long)__float_as_uint(v),
+        __hip_atomic_fetch_max(arcw + i * Vp + y, ((unsigned long long)tag << 32) | (unsigned long long)__float_as_uint(v),
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        if (L == N - 1 && j < kAux) sTN[j] = tnext;
+        if (L == Nl[i] - 1 && j < kAux) sTN[i * kAux + j] = tnext;
       }
     };
     if (ok) {
@@ -557,33 +610,39 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
       }
 #pragma unroll
-      for (int u = 0; u < kUA; ++u)
-        if (at[u] != 0) put_arc(at[u] >> 16, at[u] & 0xFFFF, ab[u], tn[u]);
+      for (int i = 0; i < NL; ++i)
+#pragma unroll
+        for (int u = 0; u < kUA; ++u)
+          if (at[i][u] != 0) put_arc(i, at[i][u] >> 16, at[i][u] & 0xFFFF, ab[i][u], tn[i][u]);
       // arcs beyond the first kUA * W of the flattened levels
-      int covered = kUA * W;
-      for (int L = 2; L <= m; ++L) {
-        const int bL = rdl(rw, rec_beg_lane(L)), cL = rdl(rw, rec_cnt_lane(L));
-        const int done = min(cL, max(0, covered));
-        covered -= cL;
-        const int2 *A = lm.arcs + bL;
-        for (int j0 = done; j0 < cL; j0 += 4 * W) {
-          int2 a4[4];
-          int t4[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int j = j0 + u * W + g;
-            a4[u] = j < cL ? A[j] : make_int2(INT_MAX, 0);
-            t4[u] = (L == N - 1 && j < cL && j < kAux) ? lm.top_next[bL + j - lm.arc_base[N - 1]] : 0;
-          }
+      for (int i = 0; i < NL; ++i) {
+        const int l0 = rec_lane0(i), N = Nl[i];
+        int covered = kUA * W;
+        for (int L = 2; L <= m[i]; ++L) {
+          const int bL = rdl(rw, l0 + rec_beg_lane(L)), cL = rdl(rw, l0 + rec_cnt_lane(L));
+          const int done = min(cL, max(0, covered));
+          covered -= cL;
+          const int2 *A = lms[i].arcs + bL;
+          for (int j0 = done; j0 < cL; j0 += 4 * W) {
+            int2 a4[4];
+            int t4[4];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const int j = j0 + u * W + g;
-            if (j < cL) put_arc(L, j, a4[u], t4[u]);
+            for (int u = 0; u < 4; ++u) {
+              const int j = j0 + u * W + g;
+              a4[u] = j < cL ? A[j] : make_int2(INT_MAX, 0);
+              t4[u] = (L == N - 1 && j < cL && j < kAux) ? lms[i].top_next[bL + j - lms[i].arc_base[N - 1]] : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int j = j0 + u * W + g;
+              if (j < cL) put_arc(i, L, j, a4[u], t4[u]);
+            }
           }
         }
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);  // the dense row has landed in LDS
+    __builtin_amdgcn_s_waitcnt(0);  // the dense rows have landed in LDS
     __syncthreads();
     // ---- combine the row statistics (lanes 0..NW-1 hold one wave each) --------------
     float lse;
@@ -625,12 +684,17 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
       if (want_keys) {
         const uint4 p4 = *reinterpret_cast<const uint4 *>(ptag + y0);
-        const uint4 a01 = *reinterpret_cast<const uint4 *>(arcw + y0);
-        const uint4 a23 = *reinterpret_cast<const uint4 *>(arcw + y0 + 2);
-        const float4 l4 = *reinterpret_cast<const float4 *>(lmval + y0);
-        const uint32_t aw[4] = {a01.y, a01.w, a23.y, a23.w};  // tag halves of the arc entries
-        const uint32_t av[4] = {a01.x, a01.z, a23.x, a23.z};  // value halves
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+        uint32_t aw[NL][4], av[NL][4];  // tag and value halves of the arc entries
+        float lv[NL][4];                // dense rows
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const uint4 a01 = *reinterpret_cast<const uint4 *>(arcw + i * Vp + y0);
+          const uint4 a23 = *reinterpret_cast<const uint4 *>(arcw + i * Vp + y0 + 2);
+          const float4 l4 = *reinterpret_cast<const float4 *>(lmval + i * Vp + y0);
+          aw[i][0] = a01.y; aw[i][1] = a01.w; aw[i][2] = a23.y; aw[i][3] = a23.w;
+          av[i][0] = a01.x; av[i][1] = a01.z; av[i][2] = a23.x; av[i][3] = a23.z;
+          lv[i][0] = l4.x; lv[i][1] = l4.y; lv[i][2] = l4.z; lv[i][3] = l4.w;
+        }
         // transition + 1 of this frame's phrase entry, 0 if none
         uint32_t hi[4];
 #pragma unroll
@@ -650,27 +714,38 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           for (int j = 0; j < 4; ++j)
             if (hi[j] > (uint32_t)kAux) eh[j] = as_float(tr.delta[dbeg + (int)hi[j] - 1].z);
         }
-        // the dense row plus the backoffs of levels 2..m in increasing order (the
-        // levels above m back off by 0)
-        float dres[4] = {lv[0], lv[1], lv[2], lv[3]};
-        for (int L2 = 2; L2 <= m; ++L2) {
-          const float b2 = as_float(rdl(rw, rec_bo_lane(L2)));
+        // per LM, the dense row plus the backoffs of levels 2..m in increasing
+        // order (the levels above m back off by 0)
+        float dres[NL][4];
 #pragma unroll
-          for (int j = 0; j < 4; ++j) dres[j] = dres[j] + b2;
+        for (int i = 0; i < NL; ++i) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) dres[i][j] = lv[i][j];
+          for (int L2 = 2; L2 <= m[i]; ++L2) {
+            const float b2 = as_float(rdl(rw, rec_lane0(i) + rec_bo_lane(L2)));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) dres[i][j] = dres[i][j] + b2;
+          }
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int y = y0 + j;
           const float x = xv[c][j];
-          // LM: this frame's winning arc if there is one, else the backed-off dense row
-          const float lmv = (aw[j] >> 16) == stamp ? __uint_as_float(av[j]) : dres[j];
+          // the LM terms in model order: u = (x + a_1 lm_1) + a_2 lm_2 ..., each LM
+          // its winning arc of this frame if there is one, else its backed-off
+          // dense row
+          float u = x;
+#pragma unroll
+          for (int i = 0; i < NL; ++i) {
+            const float lmv = (aw[i][j] >> 16) == stamp ? __uint_as_float(av[i][j]) : dres[i][j];
+            const float a1 = p.lam[i] * lmv;
+            u = u + a1;
+          }
           // phrases: the transition's entry value if this state overrides y, else the root's
           const float e = hi[j] ? eh[j] : rE[c][j];
           const float bst = e - phiq;
-          const float a1 = p.lam * lmv;
-          const float a2 = x + a1;
           const float a3 = p.beta * (p.has_trie ? bst : 0.0f);
-          kk[c][j] = (y == blank) ? x : a2 + a3;
+          kk[c][j] = (y == blank) ? x : u + a3;
         }
       }
       if (write_fused && y0 < V) {
@@ -749,9 +824,13 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       unsigned long long by = 4ull * V;
       if (ok) {
         const unsigned long long row = 4ull * V;
-        by += umin64(8ull * (unsigned long long)lm.cnt1[c1], row);
-        for (int L2 = 2; L2 <= m; ++L2) by += umin64(8ull * (unsigned long long)rdl(rw, rec_cnt_lane(L2)), row) + 12ull;
-        if (m >= 2) by += 8ull;
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          by += umin64(8ull * (unsigned long long)lms[i].cnt1[c1[i]], row);
+          for (int L2 = 2; L2 <= m[i]; ++L2)
+            by += umin64(8ull * (unsigned long long)rdl(rw, rec_lane0(i) + rec_cnt_lane(L2)), row) + 12ull;
+          if (m[i] >= 2) by += 8ull;
+        }
         if (p.has_trie) by += 16ull + 16ull * (unsigned long long)dcnt;
       }
       by += MODE == kModeBeam ? 8ull : 4ull;
@@ -809,19 +888,26 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
       // each candidate lane resolves where its next state comes from (see HypState)
       const float cf = cy != INT_MAX ? key_of(ck) - lse : -INFINITY;
-      int cl = sid, cq = qid;
+      int cl[NL], cq = qid;
+#pragma unroll
+      for (int i = 0; i < NL; ++i) cl[i] = sid[i];
       if (cy != INT_MAX && cy != blank) {
-        // the token's LDS entries of this frame: LM winner level / offset, phrase transition
-        const uint32_t aw = (uint32_t)(arcw[cy] >> 32), pw = ptag[cy];
-        const uint32_t lo = (aw >> 16) == stamp ? (aw & 0xFFFFu) : 0u;
-        const uint32_t hi = (pw >> 16) == stamp ? (pw & 0xFFFFu) : 0u;
-        cl = -1;
-        if (lo) {
-          const int L = (int)(lo >> 13), jj = (int)(lo & 0x1FFFu);
-          const int bL = s_lbeg[L];
-          cl = L < N - 1 ? (int)(s_sbase[L] + bL + jj)
-                         : (jj < kAux ? sTN[jj] : lm.top_next[bL + jj - lm.arc_base[N - 1]]);
+        // the token's LDS entries of this frame: per LM the winner's level /
+        // offset, the phrase transition
+#pragma unroll
+        for (int i = 0; i < NL; ++i) {
+          const uint32_t aw = (uint32_t)(arcw[i * Vp + cy] >> 32);
+          const uint32_t lo = (aw >> 16) == stamp ? (aw & 0xFFFFu) : 0u;
+          cl[i] = -1;
+          if (lo) {
+            const int L = (int)(lo >> 13), jj = (int)(lo & 0x1FFFu), N = Nl[i];
+            const int bL = s_lbeg[i][L];
+            cl[i] = L < N - 1 ? (int)(s_sbase[i][L] + bL + jj)
+                              : (jj < kAux ? sTN[i * kAux + jj] : lms[i].top_next[bL + jj - lms[i].arc_base[N - 1]]);
+          }
         }
+        const uint32_t pw = ptag[cy];
+        const uint32_t hi = (pw >> 16) == stamp ? (pw & 0xFFFFu) : 0u;
         cq = -1;
         if (hi) {
           // LDS copy for the first kAux transitions, the table beyond; the table is
@@ -839,54 +925,66 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           if (cy == INT_MAX) {
             p.tokens[o] = -1;
             p.scores[o] = -INFINITY;
-            p.next_lm[o] = hs.cur_lm;
+#pragma unroll
+            for (int i = 0; i < NL; ++i) p.next_lm[(int64_t)i * H * K + o] = hs.cur_lm[i];  // [n_lm][H][k]
             p.next_boost[o] = hs.cur_q;
           } else {
-            int l = cl, q = cq;
-            if (!inv && l < 0) l = lm.rec_dense[((int64_t)hs.c1 * V + cy) * RS + 1];
+            int q = cq;
+#pragma unroll
+            for (int i = 0; i < NL; ++i) {
+              int l = cl[i];
+              if (!inv && l < 0) l = lms[i].rec_dense[((int64_t)hs.c1[i] * V + cy) * RSl[i] + 1];
+              p.next_lm[(int64_t)i * H * K + o] = l;
+            }
             if (!inv && q < 0) q = tr.root_node[cy].w;
             p.tokens[o] = cy;
             p.scores[o] = cf;
-            p.next_lm[o] = l;
             p.next_boost[o] = q;
           }
         }
       } else if (MODE == kModeGreedy) {
         if (lane == 0) {
-          const int c1p = hs.c1;
           p.tokens[(int64_t)t * H + h] = cy;
-          hs.lmsrc = cl;
+#pragma unroll
+          for (int i = 0; i < NL; ++i) {
+            const int c1p = hs.c1[i];
+            hs.lmsrc[i] = cl[i];
+            hs.c1p[i] = c1p;
+            hs.c1[i] = cy != blank ? cy : c1p;
+          }
           hs.qsrc = cq;
           hs.y = cy;
-          hs.c1p = c1p;
-          hs.c1 = cy != blank ? cy : c1p;
         }
       } else {
         // ---- beam: publish this hypothesis' candidates, meet the stream, rank all ----
-        // A candidate record is four 64-bit words, each carrying the frame tag in
-        // its top 16 bits over 48 bits of payload: the total score S_b + fused
-        // (fp64), the LM and phrase sources, the token and the parent's c_1 and
-        // flags.  Words are written and read as relaxed agent-scope atomics, so a
-        // reader that sees the current tag in all four words holds the whole
-        // record: polling the records is the rendezvous (no counter, no fence).
-        // Frames alternate between two buffers; a writer can be at most one frame
-        // ahead of any reader of its stream, so it never overwrites a buffer that
-        // is still being read.
-        unsigned long long *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * 4;
+        // A candidate record is XW = 3 + NL 64-bit words, each carrying the frame
+        // tag in its top 16 bits over 48 bits of payload: the total score S_b +
+        // fused (fp64), the first LM's and the phrase source, the token, the
+        // parent's c_1 (first LM) and flags, and for a second LM its source and
+        // the parent's c_1.  Words are written and read as relaxed agent-scope
+        // atomics, so a reader that sees the current tag in all words holds the
+        // whole record: polling the records is the rendezvous (no counter, no
+        // fence).  Frames alternate between two buffers; a writer can be at most
+        // one frame ahead of any reader of its stream, so it never overwrites a
+        // buffer that is still being read.
+        constexpr int XW = 3 + NL;
+        unsigned long long *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * XW;
         const unsigned long long tag = (unsigned long long)((t + 1) & 0xFFFF) << 48;
         constexpr unsigned long long kPay = (1ull << 48) - 1;
         if (lane < K) {
           const bool has = act && cy != INT_MAX;
           const double tot = has ? hs.S + (double)cf : -INFINITY;
           const unsigned long long tb = (unsigned long long)__double_as_longlong(tot);
-          const unsigned long long w[4] = {
-              (tb & kPay) | tag,
-              (tb >> 48) | ((unsigned long long)(unsigned)cl << 16) | tag,
-              (unsigned long long)(unsigned)cq | ((unsigned long long)(has ? cy + 1 : 0) << 32) | tag,
-              (unsigned long long)((hs.c1 + 1) & 0xFFFF) | ((unsigned long long)(hs.fl & 0xFF) << 16) | tag};
+          unsigned long long w[XW];
+          w[0] = (tb & kPay) | tag;
+          w[1] = (tb >> 48) | ((unsigned long long)(unsigned)cl[0] << 16) | tag;
+          w[2] = (unsigned long long)(unsigned)cq | ((unsigned long long)(has ? cy + 1 : 0) << 32) | tag;
+          w[3] = (unsigned long long)((hs.c1[0] + 1) & 0xFFFF) | ((unsigned long long)(hs.fl & 0xFF) << 16) | tag;
+          if constexpr (NL > 1)
+            w[4] = (unsigned long long)(unsigned)cl[1] | ((unsigned long long)((hs.c1[1] + 1) & 0xFFFF) << 32) | tag;
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            __hip_atomic_store(xs + (b * K + lane) * 4 + q, w[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          for (int q = 0; q < XW; ++q)
+            __hip_atomic_store(xs + (b * K + lane) * XW + q, w[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         // every workgroup of the stream ranks the same B*k candidates by (total
         // desc, parent asc, rank asc), i.e. candidate order breaks ties; slot b
@@ -895,13 +993,17 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const int nc = B * K;
         for (int i0 = 0; i0 < nc; i0 += 64) {
           const int i = i0 + lane;
-          unsigned long long w[4] = {0ull, 0ull, 0ull, 0ull};
+          unsigned long long w[XW];
+#pragma unroll
+          for (int q = 0; q < XW; ++q) w[q] = 0ull;
           bool cur = i >= nc;
           for (int spins = 0;; ++spins) {
             if (i < nc) {
 #pragma unroll
-              for (int q = 0; q < 4; ++q) w[q] = __hip_atomic_load(xs + i * 4 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              cur = (w[0] & ~kPay) == tag && (w[1] & ~kPay) == tag && (w[2] & ~kPay) == tag && (w[3] & ~kPay) == tag;
+              for (int q = 0; q < XW; ++q) w[q] = __hip_atomic_load(xs + i * XW + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              cur = true;
+#pragma unroll
+              for (int q = 0; q < XW; ++q) cur = cur && (w[q] & ~kPay) == tag;
             }
             if (__ballot(!cur) == 0ull || aborted) break;
             if (spins >= kSpinLimit) {
@@ -917,6 +1019,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             s_xa[i] = make_int4(y1 - 1, (int)(unsigned)((w[1] >> 16) & 0xFFFFFFFFull), (int)(unsigned)(w[2] & 0xFFFFFFFFull),
                                 (int)(w[3] & 0xFFFF) - 1);
             s_xf[i] = (int)((w[3] >> 16) & 0xFF);
+            if constexpr (NL > 1)
+              s_xb[i] = make_int2((int)(unsigned)(w[4] & 0xFFFFFFFFull), (int)((w[4] >> 32) & 0xFFFF) - 1);
             s_tot[i] = valid ? __longlong_as_double((long long)((w[0] & kPay) | ((w[1] & 0xFFFF) << 48)))
                              : __longlong_as_double(0x7FF8000000000000ll);
           }
@@ -941,12 +1045,23 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         if (wi >= 0) {
           // the lane holding the slot's candidate installs it
           const int4 a = s_xa[wi];
-          const int y = a.x, c1p = a.w;
-          hs.lmsrc = a.y;
+          const int y = a.x;
+          int src[NL], c1p[NL];
+          src[0] = a.y;
+          c1p[0] = a.w;
+          if constexpr (NL > 1) {
+            const int2 xb = s_xb[wi];
+            src[1] = xb.x;
+            c1p[1] = xb.y;
+          }
+#pragma unroll
+          for (int i = 0; i < NL; ++i) {
+            hs.lmsrc[i] = src[i];
+            hs.c1p[i] = c1p[i];
+            hs.c1[i] = y != blank ? y : c1p[i];
+          }
           hs.qsrc = a.z;
           hs.y = y;
-          hs.c1p = c1p;
-          hs.c1 = y != blank ? y : c1p;
           hs.fl = 1 | (s_xf[wi] & 2);
           hs.S = s_tot[wi];
           p.tokens[o] = y;
@@ -954,10 +1069,13 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
         if (__ballot(wi >= 0) == 0ull && lane == 0) {
           // no candidate reaches this slot: the hypothesis is dead and keeps its state
-          hs.lmsrc = hs.cur_lm;
+#pragma unroll
+          for (int i = 0; i < NL; ++i) {
+            hs.lmsrc[i] = hs.cur_lm[i];
+            hs.c1p[i] = -1;
+          }
           hs.qsrc = hs.cur_q;
           hs.y = -1;
-          hs.c1p = -1;
           hs.fl = 0;
           hs.S = -INFINITY;
           p.tokens[o] = -1;
@@ -970,14 +1088,18 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   // ---- final state ----------------------------------------------------------------
   if (MODE != kModeStep && g == 0) {
     const int V = p.V;
-    int nl = hs.lmsrc, nq = hs.qsrc;
+    int nq = hs.qsrc;
     const int y = hs.y;
     // a negative source means "reached by token y" only for valid hypotheses
     // that made a transition; an invalid hypothesis keeps its raw ids
     const bool moved = (hs.fl & 2) == 0 && y >= 0 && y != p.blank;
-    if (moved && nl < 0) nl = lm.rec_dense[((int64_t)hs.c1p * V + y) * RS + 1];
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      int nl = hs.lmsrc[i];
+      if (moved && nl < 0) nl = lms[i].rec_dense[((int64_t)hs.c1p[i] * V + y) * RSl[i] + 1];
+      p.lm_state[(int64_t)i * H + h] = nl;
+    }
     if (moved && nq < 0) nq = tr.root_node[y].w;
-    p.lm_state[h] = nl;
     if (p.has_trie) p.boost_state[h] = nq;
     if (MODE == kModeBeam) p.hyp_score[h] = hs.S;
   }
@@ -997,20 +1119,20 @@ __global__ void zero_ints(int *p, int n) {
 // ---------------------------------------------------------------------------
 typedef void (*KernelFn)(Params);
 
-template <int W, int NC, int KM, bool AL>
+template <int W, int NC, int KM, bool AL, int NL>
 KernelFn pick_mode(int mode) {
   if constexpr (KM == 1) {
-    if (mode == kModeGreedy) return fusion_kernel<W, NC, KM, AL, kModeGreedy>;
+    if (mode == kModeGreedy) return fusion_kernel<W, NC, KM, AL, kModeGreedy, NL>;
   }
-  return mode == kModeStep ? fusion_kernel<W, NC, KM, AL, kModeStep> : fusion_kernel<W, NC, KM, AL, kModeBeam>;
+  return mode == kModeStep ? fusion_kernel<W, NC, KM, AL, kModeStep, NL> : fusion_kernel<W, NC, KM, AL, kModeBeam, NL>;
 }
-template <int W, int NC, int KM>
+template <int W, int NC, int KM, int NL>
 KernelFn pick_al(bool al, int mode) {
-  return al ? pick_mode<W, NC, KM, true>(mode) : pick_mode<W, NC, KM, false>(mode);
+  return al ? pick_mode<W, NC, KM, true, NL>(mode) : pick_mode<W, NC, KM, false, NL>(mode);
 }
-template <int W, int NC>
+template <int W, int NC, int NL>
 KernelFn pick_k(int km, bool al, int mode) {
-  return km == 1 ? pick_al<W, NC, 1>(al, mode) : km == 4 ? pick_al<W, NC, 4>(al, mode) : pick_al<W, NC, 8>(al, mode);
+  return km == 1 ? pick_al<W, NC, 1, NL>(al, mode) : km == 4 ? pick_al<W, NC, 4, NL>(al, mode) : pick_al<W, NC, 8, NL>(al, mode);
 }
 
 struct Shape {
@@ -1025,11 +1147,25 @@ Shape shape_for(int V) {
   return {1024, 2, 8192};
 }
 
-KernelFn pick(const Shape &sh, int km, bool al, int mode) {
-  if (sh.W == 64) return pick_k<64, 1>(km, al, mode);
-  if (sh.W == 256) return pick_k<256, 1>(km, al, mode);
-  if (sh.NC == 1) return pick_k<1024, 1>(km, al, mode);
-  return pick_k<1024, 2>(km, al, mode);
+// two LMs are compiled for vocabularies up to 4096 (two LMs at 8192 need more
+// LDS than a workgroup has)
+KernelFn pick(const Shape &sh, int km, bool al, int mode, int n_lm) {
+  if (n_lm == 2) {
+    if (sh.W == 64) return pick_k<64, 1, 2>(km, al, mode);
+    if (sh.W == 256) return pick_k<256, 1, 2>(km, al, mode);
+    if (sh.NC == 1) return pick_k<1024, 1, 2>(km, al, mode);
+    return nullptr;
+  }
+  if (sh.W == 64) return pick_k<64, 1, 1>(km, al, mode);
+  if (sh.W == 256) return pick_k<256, 1, 1>(km, al, mode);
+  if (sh.NC == 1) return pick_k<1024, 1, 1>(km, al, mode);
+  return pick_k<1024, 2, 1>(km, al, mode);
+}
+
+// dynamic LDS of a launch: per LM the dense row and the arc entries, the phrase
+// entries, the phrase side tables and per LM the top-level next states
+size_t dyn_lds_bytes(int Vp, int n_lm) {
+  return (size_t)Vp * (12 * n_lm + 4) + (size_t)4 * (kAux * (2 + n_lm) + 4);
 }
 
 struct DeviceInfo {
@@ -1059,10 +1195,11 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   const int km = p.k <= 1 ? 1 : p.k <= 4 ? 4 : 8;
   const bool al = (p.V % 4 == 0) && ((uintptr_t)p.logits % 16 == 0) && (!p.fused || (uintptr_t)p.fused % 16 == 0);
   const int mode = p.step_mode ? kModeStep : p.B == 1 ? kModeGreedy : kModeBeam;
-  KernelFn fn = pick(sh, km, al, mode);
+  KernelFn fn = pick(sh, km, al, mode, p.n_lm);
+  if (!fn) return set_error(FUSION_E_UNSUPPORTED, "two LMs need V <= 4096");
   const DeviceInfo di = device_info();
   if (!di.ok) return set_error(FUSION_E_HIP, "cannot query the device");
-  const size_t dyn = (size_t)4 * (4 * sh.Vp + 3 * kAux + 4);
+  const size_t dyn = dyn_lds_bytes(sh.Vp, p.n_lm);
   hipFuncAttributes attr;
   hipError_t e = hipFuncGetAttributes(&attr, reinterpret_cast<const void *>(fn));
   if (e != hipSuccess) return hip_error(e, "hipFuncGetAttributes");
@@ -1086,8 +1223,8 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   int s_batch = (int)std::min<long>(p.S, resident / p.B);
   if (s_batch >= 8) s_batch -= s_batch % 8;
   if (s_batch < 1) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device at once");
-  // exchange records: 2 buffers x B x k candidates x 4 words per stream
-  const size_t xwords = (size_t)s_batch * 2 * p.B * p.k * 4;
+  // exchange records: 2 buffers x B x k candidates x (3 + n_lm) words per stream
+  const size_t xwords = (size_t)s_batch * 2 * p.B * p.k * (3 + p.n_lm);
   void *scratch = nullptr;
   e = hipMallocAsync(&scratch, xwords * sizeof(unsigned long long), stream);
   if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
@@ -1117,28 +1254,101 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   return rc;
 }
 
-int check_common(const NgramTables *lm, const BoostTrie *trie, const float *logits, int32_t V,
-                 int32_t k, int32_t blank_id, int32_t blank_mode, float lambda, float beta) {
-  if (!lm) return set_error(FUSION_E_ARG, "NULL n-gram tables");
+int check_common(const NgramTables *const *lms, const float *alphas, int32_t n_lm, const BoostTrie *trie,
+                 const float *logits, int32_t V, int32_t k, int32_t blank_id, int32_t blank_mode, float beta) {
+  if (n_lm < 1 || n_lm > FUSION_MAX_LMS) return set_error(FUSION_E_ARG, "n_lm out of range");
+  if (!lms || !alphas) return set_error(FUSION_E_ARG, "NULL LM list or weights");
+  for (int i = 0; i < n_lm; ++i) {
+    if (!lms[i]) return set_error(FUSION_E_ARG, "NULL n-gram tables");
+    if (V != lms[i]->dev.V) return set_error(FUSION_E_ARG, "V does not match the n-gram tables");
+    if (blank_id != lms[i]->dev.blank) return set_error(FUSION_E_ARG, "blank_id does not match the n-gram tables");
+    if (!std::isfinite(alphas[i])) return set_error(FUSION_E_ARG, "non-finite fusion weight");
+  }
   if (!logits) return set_error(FUSION_E_ARG, "NULL logits");
-  if (V != lm->dev.V) return set_error(FUSION_E_ARG, "V does not match the n-gram tables");
-  if (blank_id != lm->dev.blank) return set_error(FUSION_E_ARG, "blank_id does not match the n-gram tables");
   if (trie && (trie->dev.V != V || trie->dev.blank != blank_id))
     return set_error(FUSION_E_ARG, "phrase tree built for another vocabulary or blank");
   if (k < 1 || k > FUSION_MAX_K || k > V) return set_error(FUSION_E_ARG, "k out of range");
   if (blank_mode != FUSION_BLANK_AM && blank_mode != FUSION_BLANK_COMPETE) return set_error(FUSION_E_ARG, "unknown blank_mode");
   if (blank_mode == FUSION_BLANK_AM && k != 1) return set_error(FUSION_E_ARG, "FUSION_BLANK_AM needs k == 1");
-  if (!std::isfinite(lambda) || !std::isfinite(beta)) return set_error(FUSION_E_ARG, "non-finite fusion weight");
+  if (!std::isfinite(beta)) return set_error(FUSION_E_ARG, "non-finite fusion weight");
   return FUSION_OK;
 }
 
-Params make_params(const NgramTables *lm, const BoostTrie *trie) {
+Params make_params(const NgramTables *const *lms, const float *alphas, int32_t n_lm, const BoostTrie *trie) {
   Params p;
   std::memset(&p, 0, sizeof p);
-  p.lm = lm->dev;
+  for (int i = 0; i < n_lm; ++i) {
+    p.lm[i] = lms[i]->dev;
+    p.lam[i] = alphas[i];
+  }
+  p.n_lm = n_lm;
   if (trie) p.tr = trie->dev;
   p.has_trie = trie != nullptr;
   return p;
+}
+
+int step_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, const BoostTrie *trie,
+              const float *logits, const int32_t *lm_state, const int32_t *boost_state, int32_t H, int32_t V,
+              float beta, int32_t blank_id, int32_t k, int32_t blank_mode, float *fused, int32_t *tokens,
+              float *scores, int32_t *next_lm, int32_t *next_boost, hipStream_t stream) {
+  int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta);
+  if (rc != FUSION_OK) return rc;
+  if (H < 1 || H > (1 << 24)) return set_error(FUSION_E_ARG, "H out of range");
+  if (!lm_state || !tokens || !scores || !next_lm || !next_boost || (trie && !boost_state))
+    return set_error(FUSION_E_ARG, "NULL state or output buffer");
+  Params p = make_params(lms, alphas, n_lm, trie);
+  p.logits = logits;
+  p.lm_state = const_cast<int32_t *>(lm_state);
+  p.boost_state = const_cast<int32_t *>(boost_state);
+  p.tokens = tokens;
+  p.scores = scores;
+  p.next_lm = next_lm;
+  p.next_boost = next_boost;
+  p.fused = fused;
+  p.T = 1;
+  p.S = H;
+  p.B = 1;
+  p.V = V;
+  p.k = k;
+  p.blank = blank_id;
+  p.mode = blank_mode;
+  p.step_mode = 1;
+  p.beta = beta;
+  return launch(p, H, stream);
+}
+
+int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, const BoostTrie *trie,
+             const float *logits, int32_t T, int32_t S, int32_t B, int32_t V, int32_t k, float beta,
+             int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state, double *hyp_score,
+             int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, hipStream_t stream) {
+  int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta);
+  if (rc != FUSION_OK) return rc;
+  if (T < 0 || S < 1 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
+  if ((int64_t)S * B > (1 << 24)) return set_error(FUSION_E_ARG, "too many hypotheses");
+  if (B == 1 && k != 1) return set_error(FUSION_E_ARG, "greedy decoding (B == 1) needs k == 1");
+  if (B > 1 && blank_mode != FUSION_BLANK_COMPETE) return set_error(FUSION_E_ARG, "beam decoding needs FUSION_BLANK_COMPETE");
+  if (!lm_state || !tokens || (trie && !boost_state)) return set_error(FUSION_E_ARG, "NULL state or output buffer");
+  if (B > 1 && (!hyp_score || !parents)) return set_error(FUSION_E_ARG, "beam decoding needs hyp_score and parents");
+  if (T == 0) return FUSION_OK;
+  Params p = make_params(lms, alphas, n_lm, trie);
+  p.logits = logits;
+  p.lm_state = lm_state;
+  p.boost_state = boost_state;
+  p.hyp_score = hyp_score;
+  p.tokens = tokens;
+  p.parents = parents;
+  p.fused = fused;
+  p.traffic = traffic;
+  p.T = T;
+  p.S = S;
+  p.B = B;
+  p.V = V;
+  p.k = k;
+  p.blank = blank_id;
+  p.mode = blank_mode;
+  p.step_mode = 0;
+  p.beta = beta;
+  return launch(p, S * B, stream);
 }
 
 }  // namespace
@@ -1167,31 +1377,17 @@ extern "C" int fusion_step(const NgramTables *lm, const BoostTrie *trie, const f
                            float lambda, float beta, int32_t blank_id, int32_t k, int32_t blank_mode,
                            float *fused, int32_t *tokens, float *scores, int32_t *next_lm,
                            int32_t *next_boost, hipStream_t stream) {
-  int rc = check_common(lm, trie, logits, V, k, blank_id, blank_mode, lambda, beta);
-  if (rc != FUSION_OK) return rc;
-  if (H < 1 || H > (1 << 24)) return set_error(FUSION_E_ARG, "H out of range");
-  if (!lm_state || !tokens || !scores || !next_lm || !next_boost || (trie && !boost_state))
-    return set_error(FUSION_E_ARG, "NULL state or output buffer");
-  Params p = make_params(lm, trie);
-  p.logits = logits;
-  p.lm_state = const_cast<int32_t *>(lm_state);
-  p.boost_state = const_cast<int32_t *>(boost_state);
-  p.tokens = tokens;
-  p.scores = scores;
-  p.next_lm = next_lm;
-  p.next_boost = next_boost;
-  p.fused = fused;
-  p.T = 1;
-  p.S = H;
-  p.B = 1;
-  p.V = V;
-  p.k = k;
-  p.blank = blank_id;
-  p.mode = blank_mode;
-  p.step_mode = 1;
-  p.lam = lambda;
-  p.beta = beta;
-  return launch(p, H, stream);
+  return step_impl(&lm, &lambda, 1, trie, logits, lm_state, boost_state, H, V, beta, blank_id, k, blank_mode,
+                   fused, tokens, scores, next_lm, next_boost, stream);
+}
+
+extern "C" int fusion_step_lms(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
+                               const BoostTrie *trie, const float *logits, const int32_t *lm_state,
+                               const int32_t *boost_state, int32_t H, int32_t V, float beta, int32_t blank_id,
+                               int32_t k, int32_t blank_mode, float *fused, int32_t *tokens, float *scores,
+                               int32_t *next_lm, int32_t *next_boost, hipStream_t stream) {
+  return step_impl(lms, alphas, n_lm, trie, logits, lm_state, boost_state, H, V, beta, blank_id, k, blank_mode,
+                   fused, tokens, scores, next_lm, next_boost, stream);
 }
 
 extern "C" int fusion_run(const NgramTables *lm, const BoostTrie *trie, const float *logits, int32_t T,
@@ -1199,33 +1395,15 @@ extern "C" int fusion_run(const NgramTables *lm, const BoostTrie *trie, const fl
                           int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state,
                           double *hyp_score, int32_t *tokens, int32_t *parents, float *fused,
                           int64_t *traffic, hipStream_t stream) {
-  int rc = check_common(lm, trie, logits, V, k, blank_id, blank_mode, lambda, beta);
-  if (rc != FUSION_OK) return rc;
-  if (T < 0 || S < 1 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
-  if ((int64_t)S * B > (1 << 24)) return set_error(FUSION_E_ARG, "too many hypotheses");
-  if (B == 1 && k != 1) return set_error(FUSION_E_ARG, "greedy decoding (B == 1) needs k == 1");
-  if (B > 1 && blank_mode != FUSION_BLANK_COMPETE) return set_error(FUSION_E_ARG, "beam decoding needs FUSION_BLANK_COMPETE");
-  if (!lm_state || !tokens || (trie && !boost_state)) return set_error(FUSION_E_ARG, "NULL state or output buffer");
-  if (B > 1 && (!hyp_score || !parents)) return set_error(FUSION_E_ARG, "beam decoding needs hyp_score and parents");
-  if (T == 0) return FUSION_OK;
-  Params p = make_params(lm, trie);
-  p.logits = logits;
-  p.lm_state = lm_state;
-  p.boost_state = boost_state;
-  p.hyp_score = hyp_score;
-  p.tokens = tokens;
-  p.parents = parents;
-  p.fused = fused;
-  p.traffic = traffic;
-  p.T = T;
-  p.S = S;
-  p.B = B;
-  p.V = V;
-  p.k = k;
-  p.blank = blank_id;
-  p.mode = blank_mode;
-  p.step_mode = 0;
-  p.lam = lambda;
-  p.beta = beta;
-  return launch(p, S * B, stream);
+  return run_impl(&lm, &lambda, 1, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
+                  boost_state, hyp_score, tokens, parents, fused, traffic, stream);
+}
+
+extern "C" int fusion_run_lms(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
+                              const BoostTrie *trie, const float *logits, int32_t T, int32_t S, int32_t B,
+                              int32_t V, int32_t k, float beta, int32_t blank_id, int32_t blank_mode,
+                              int32_t *lm_state, int32_t *boost_state, double *hyp_score, int32_t *tokens,
+                              int32_t *parents, float *fused, int64_t *traffic, hipStream_t stream) {
+  return run_impl(lms, alphas, n_lm, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
+                  boost_state, hyp_score, tokens, parents, fused, traffic, stream);
 }

@@ -117,3 +117,19 @@ def test_fusion_calls_reject_bad_arguments(lib):
                         None, None, None, None)
     assert rc == F.FUSION_E_ARG
     assert "NULL" in F.fusion_last_error()
+
+
+def test_several_lm_calls_reject_bad_arguments(lib):
+    out = [None] * 5
+    al = (ctypes.c_float * 3)(0.5, 0.5, 0.5)
+    hs = (ctypes.c_void_p * 3)(None, None, None)
+    for n in (0, F.FUSION_MAX_LMS + 1):
+        rc = lib.fusion_step_lms(ctypes.cast(hs, ctypes.c_void_p), ctypes.cast(al, ctypes.c_void_p), n,
+                                 None, None, None, None, 1, 4, 0.5, 0, 1, 0, *out, None)
+        assert rc == F.FUSION_E_ARG and "n_lm" in F.fusion_last_error()
+    rc = lib.fusion_step_lms(None, None, 2, None, None, None, None, 1, 4, 0.5, 0, 1, 0, *out, None)
+    assert rc == F.FUSION_E_ARG
+    rc = lib.fusion_run_lms(ctypes.cast(hs, ctypes.c_void_p), ctypes.cast(al, ctypes.c_void_p), 2, None,
+                            None, 1, 1, 1, 4, 1, 0.5, 0, 0, None, None, None, None, None, None, None,
+                            None)
+    assert rc == F.FUSION_E_ARG and "NULL" in F.fusion_last_error()

@@ -1,0 +1,165 @@
+"""GPU parity of the several-LM form of Eq. (1) (Sec. III-C: one weighted LM
+term per model, each model with its own state) against the oracle's
+``step_lms`` / ``run_lms``.  Same bar as the one-LM path: tokens, top-k sets
+and every LM's next state bit-exact, fp32 fused scores within 1e-5, beam
+merges exact except accepted near ties."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_14991_amd as F
+from workloads import load_workload, tiny_random_lm, tiny_random_phrases
+
+pytestmark = pytest.mark.gpu
+
+SCORE_TOL = 1e-5
+TIE_TOL = 1e-4
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def random_states(lm, n, rng):
+    """n LM state ids over every order of context (plus <s>)."""
+    V = lm.vocab
+    ids = [V] + [int(t) for t in lm.tokens[0][:, 0] if t != V + 1 and t != lm.blank]
+    off = V + 2
+    for k in range(2, lm.order):
+        nk = lm.tokens[k - 1].shape[0]
+        ids += [off + i for i in range(nk) if lm.tokens[k - 1][i, -1] != V + 1]
+        off += nk
+    return rng.choice(np.array(ids, dtype=np.int64), size=n).astype(np.int32)
+
+
+def check_step(lms_arr, ph, x, states, bs, alphas, beta, k, mode, label):
+    V = x.shape[1]
+    glms = [F.ngram_load_arrays(m) for m in lms_arr]
+    gtr = F.boost_build_phrases(V, 0, ph)
+    olms = [oracle.OracleLM(m) for m in lms_arr]
+    otr = oracle.OracleTrie(V, 0, ph)
+    g = F.step_lms(glms, alphas, gtr, torch.from_numpy(x).to(dev()), torch.from_numpy(states).to(dev()),
+                   torch.from_numpy(bs).to(dev()), beta, 0, k, mode, want_fused=True)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.step_lms(olms, alphas, otr, x, states, bs, beta, 0, k, mode)
+    assert np.array_equal(g["tokens"].cpu().numpy(), r["tokens"]), f"{label}: tokens"
+    assert np.array_equal(g["next_lm"].cpu().numpy(), r["next_lm"]), f"{label}: next LM states"
+    assert np.array_equal(g["next_boost"].cpu().numpy(), r["next_boost"]), f"{label}: next phrase states"
+    err = np.abs(g["fused"].cpu().numpy().astype(np.float64) - r["fused"]).max()
+    assert err <= SCORE_TOL, f"{label}: fused max err {err}"
+    serr = np.abs(g["scores"].cpu().numpy().astype(np.float64) - r["scores"]).max()
+    assert serr <= SCORE_TOL, f"{label}: scores max err {serr}"
+
+
+@pytest.mark.parametrize("V,H", [(200, 40), (1000, 64), (4000, 48)])
+def test_step_two_lms_random_states(V, H):
+    """Two LMs of different orders in random states of every order, at the three
+    workgroup shapes (64, 256 and 1024 lanes): full fused rows, top-4 in mode B
+    and the acoustic-blank mode A."""
+    rng = np.random.default_rng(V)
+    lms = [tiny_random_lm(rng, V, 4, n_sent=3000), tiny_random_lm(rng, V, 3, n_sent=1500)]
+    ph = tiny_random_phrases(rng, V, n=40, max_len=4, alphabet=min(V - 1, 30), with_completion=True)
+    x = (rng.standard_normal((H, V)) * 2).astype(np.float32)
+    x[:, 0] += 2
+    states = np.stack([random_states(m, H, rng) for m in lms])
+    nodes = oracle.OracleTrie(V, 0, ph).n_nodes
+    bs = rng.integers(0, nodes, size=H).astype(np.int32)
+    for mode, k in [(1, 4), (0, 1)]:
+        check_step(lms, ph, x, states, bs, [0.5, 0.3], 0.5, k, mode, f"V {V} mode {mode} k {k}")
+
+
+def test_second_lm_with_zero_weight_is_the_one_lm_kernel():
+    """alpha_2 = 0: the two-LM kernel's keys, selections and first-LM states
+    equal the one-LM kernel's bit for bit."""
+    w = load_workload(2, T=1)
+    rng = np.random.default_rng(4)
+    other = tiny_random_lm(rng, w.V, 3, n_sent=2000)
+    glm, glm2 = F.ngram_load_arrays(w.lm), F.ngram_load_arrays(other)
+    gtr = F.boost_build_phrases(w.V, 0, w.phrases)
+    H = 128
+    x = torch.from_numpy((rng.standard_normal((H, w.V)) * 2).astype(np.float32)).to(dev())
+    s1 = random_states(w.lm, H, rng)
+    s2 = random_states(other, H, rng)
+    bs = torch.zeros(H, dtype=torch.int32, device=dev())
+    one = F.step(glm, gtr, x, torch.from_numpy(s1).to(dev()), bs, 0.5, 0.5, 0, 4, F.FUSION_BLANK_COMPETE,
+                 want_fused=True)
+    two = F.step_lms([glm, glm2], [0.5, 0.0], gtr, x, torch.from_numpy(np.stack([s1, s2])).to(dev()), bs,
+                     0.5, 0, 4, F.FUSION_BLANK_COMPETE, want_fused=True)
+    torch.cuda.synchronize()
+    assert torch.equal(one["tokens"], two["tokens"])
+    assert torch.equal(one["fused"], two["fused"])
+    assert torch.equal(one["next_lm"], two["next_lm"][0])
+    assert torch.equal(one["next_boost"], two["next_boost"])
+
+
+def test_greedy_two_lms_free_running_c1():
+    """C1 in full with a second LM: one stream, 200 frames, greedy mode A; the
+    trajectory and both final LM states equal the oracle's."""
+    w = load_workload(1)
+    other = tiny_random_lm(np.random.default_rng(21), w.V, 4, n_sent=4000)
+    glms = [F.ngram_load_arrays(w.lm), F.ngram_load_arrays(other)]
+    gtr = F.boost_build_phrases(w.V, 0, w.phrases)
+    ls = torch.full((2, 1), w.V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((1,), dtype=torch.int32, device=dev())
+    alphas = [w.lam, 0.2]
+    out = F.run_lms(glms, alphas, gtr, torch.from_numpy(w.logits).to(dev()), 1, 1, 1, w.beta, 0,
+                    F.FUSION_BLANK_AM, ls, bs)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.run_lms([oracle.OracleLM(w.lm), oracle.OracleLM(other)], alphas,
+                       oracle.OracleTrie(w.V, 0, w.phrases), w.logits, 1, 1, 1, w.beta, 0, 0,
+                       [[w.V], [w.V]], [0])
+    tok = out["tokens"].cpu().numpy()
+    assert np.array_equal(tok, r["tokens"])
+    assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
+    assert int(bs.cpu()[0]) == r["boost_state"][0]
+    assert (tok != 0).sum() > 100
+
+
+@pytest.mark.parametrize("V,S", [(300, 24), (1100, 40)])
+def test_beam_two_lms_teacher_forced(V, S):
+    """Beam 4, top-4, 30 frames with two LMs: every decision is replayed by the
+    oracle (near ties within 1e-4 accepted); both LMs' final states, the
+    phrase states and the final scores match."""
+    rng = np.random.default_rng(70 + V)
+    B, k, T = 4, 4, 30
+    lms = [tiny_random_lm(rng, V, 4, n_sent=3000), tiny_random_lm(rng, V, 3, n_sent=2000)]
+    ph = tiny_random_phrases(rng, V, n=40, max_len=4, alphabet=min(V - 1, 30), with_completion=True)
+    glms = [F.ngram_load_arrays(m) for m in lms]
+    gtr = F.boost_build_phrases(V, 0, ph)
+    x = (rng.standard_normal((T, S * B, V)) * 2).astype(np.float32)
+    x[:, :, 0] += 2
+    H = S * B
+    alphas = [0.5, 0.25]
+    ls = torch.full((2, H), V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev())
+    sc0 = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)
+    sc = torch.from_numpy(sc0.copy()).to(dev())
+    out = F.run_lms(glms, alphas, gtr, torch.from_numpy(x).to(dev()), S, B, k, 0.5, 0,
+                    F.FUSION_BLANK_COMPETE, ls, bs, sc)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.run_lms([oracle.OracleLM(m) for m in lms], alphas, oracle.OracleTrie(V, 0, ph), x, S, B,
+                       k, 0.5, 0, 1, [[V] * H, [V] * H], [0] * H, sc0,
+                       forced_tokens=out["tokens"].cpu().numpy(),
+                       forced_parents=out["parents"].cpu().numpy(), tol=TIE_TOL, threads=8)
+    assert (r["mismatch_at"] < 0).all(), f"streams diverge at {r['mismatch_at'][r['mismatch_at'] >= 0][:5]}"
+    assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
+    assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
+    fin = np.isfinite(r["hyp_score"])
+    assert np.array_equal(np.isfinite(sc.cpu().numpy()), fin)
+    assert np.abs(sc.cpu().numpy()[fin] - r["hyp_score"][fin]).max() <= T * SCORE_TOL
+
+
+def test_two_lms_above_4096_tokens_are_unsupported():
+    rng = np.random.default_rng(1)
+    V = 5000
+    lms = [F.ngram_load_arrays(tiny_random_lm(rng, V, 2, n_sent=200)) for _ in range(2)]
+    x = torch.zeros((1, V), dtype=torch.float32, device=dev())
+    ls = torch.full((2, 1), V, dtype=torch.int32, device=dev())
+    with pytest.raises(F.FusionError) as e:
+        F.step_lms(lms, [0.5, 0.5], None, x, ls, None, 0.0, 0, 1, F.FUSION_BLANK_COMPETE)
+    assert e.value.code == F.FUSION_E_UNSUPPORTED
