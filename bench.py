@@ -84,6 +84,8 @@ def main():
     ap.add_argument("--fused", action="store_true", help="also write the full fused score rows")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-projection", action="store_true", help="skip the joint-projection measurement")
+    ap.add_argument("--no-second-lm", action="store_true",
+                    help="skip the two-LM measurement (C5 with a second, keyword 4-gram LM)")
     ap.add_argument("--cpu-frames", type=int, default=300)
     ap.add_argument("--cpu-streams", type=int, default=64)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -243,6 +245,62 @@ def main():
         }
         log(f"joint projection {M}x{N}x{K}: {pms:.3f} ms, {flops / (pms / 1e3) / 1e12:.1f} TFLOP/s")
         del a_d, w_d, b_d, o_d
+
+    # Eq. (1) with two LMs: the same decode with a second, keyword 4-gram LM
+    # (weights lambda, lambda), timed the same way; not part of the step above
+    if not args.no_second_lm and args.config == 5:
+        from workloads import make_keyword_lm
+
+        t3 = time.time()
+        lm2_arrays = make_keyword_lm(args.config)
+        lm2 = F.ngram_load_arrays(lm2_arrays)
+        n2_states, lm2_bytes = F.ngram_info(lm2)
+        log(f"second LM: {lm2_arrays.counts} n-grams, {lm2_bytes / 1e9:.2f} GB, {time.time() - t3:.1f}s")
+        lms2, alphas2 = [lm, lm2], [w.lam, w.lam]
+        ls2_0 = torch.stack([ls0, torch.full((H,), F.ngram_bos_state(lm2), dtype=torch.int32, device=dev)])
+        ls2 = ls2_0.clone()
+
+        def run2(traffic=None):
+            ls2.copy_(ls2_0)
+            bs.copy_(bs0)
+            sc.copy_(sc0)
+            F.fusion_run_lms(lms2, alphas2, trie, x, T, S, B, V, k, w.beta, w.blank, mode, ls2, bs, sc,
+                             tokens, parents if B > 1 else None, None, traffic, stream.cuda_stream)
+
+        traffic2 = torch.zeros(2, dtype=torch.int64, device=dev)
+        run2(traffic2)
+        torch.cuda.synchronize()
+        assert F.fusion_device_status() == 0
+        alg2, steps2 = (int(v) for v in traffic2.cpu())
+        for _ in range(2):
+            run2()
+        n2 = max(3, args.steps // 4)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n2)]
+        torch.cuda.synchronize()
+        for a, b in ev:
+            ls2.copy_(ls2_0)
+            bs.copy_(bs0)
+            sc.copy_(sc0)
+            a.record(stream)
+            F.fusion_run_lms(lms2, alphas2, trie, x, T, S, B, V, k, w.beta, w.blank, mode, ls2, bs, sc,
+                             tokens, parents if B > 1 else None, None, None, stream.cuda_stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        k2 = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+        ach2 = alg2 / (k2 / 1e3) / 1e9
+        out["two_lms"] = {
+            "kernel": "fusion_kernel (two LMs)", "launches": n2, "kernel_ms_per_launch": k2,
+            "value": float(T) * H * V / (k2 / 1e3), "unit": "hyp×vocab scores/s",
+            "decode_steps_per_s": T / (k2 / 1e3), "alphas": alphas2,
+            "second_lm": {"kind": "keyword 4-gram (inserted phrases in Zipf carriers)",
+                          "ngrams": int(sum(lm2_arrays.counts)), "ngrams_per_order": lm2_arrays.counts,
+                          "lm_states": n2_states, "lm_device_bytes": lm2_bytes},
+            "roofline": {"bound": "hbm", "achieved": ach2, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": ach2 / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg2,
+                         "bytes_per_hyp_step": alg2 / max(steps2, 1)},
+        }
+        log(f"two LMs: {k2:.3f} ms kernel, {alg2 / max(steps2, 1):.0f} B/hyp-step, {ach2:.1f} GB/s")
+        del lm2
 
     rec = recorded_traffic(w.name)
     digest = kernel_sources_digest()

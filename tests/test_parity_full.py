@@ -133,3 +133,39 @@ def test_c5_step_fused_rows():
     err = np.abs(g["fused"].cpu().numpy().astype(np.float64) - r["fused"]).max()
     assert err <= SCORE_TOL, f"fused max err {err}"
     assert F.fusion_device_status() == 0
+
+
+def test_c5_two_lms_full_beam():
+    """C5 with a second, keyword 4-gram LM (Eq. (1) with two weighted LM terms),
+    in the launch bench.py times: every decision of the 64 x 4 beam over 300
+    frames is replayed by the oracle; both LMs' final states and the scores match."""
+    from workloads import make_keyword_lm
+
+    w = load_workload(5)
+    lm2 = make_keyword_lm(5)
+    glms = [F.ngram_load_arrays(w.lm), F.ngram_load_arrays(lm2)]
+    trie = F.boost_build_phrases(w.V, w.blank, w.phrases)
+    S, B, k, T = w.S, w.B, w.k, w.T
+    H = S * B
+    alphas = [w.lam, w.lam]
+    ls = torch.full((2, H), w.V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev())
+    sc0 = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)
+    sc = torch.from_numpy(sc0.copy()).to(dev())
+    out = F.run_lms(glms, alphas, trie, torch.from_numpy(w.logits).to(dev()), S, B, k, w.beta, w.blank,
+                    F.FUSION_BLANK_COMPETE, ls, bs, sc)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.run_lms([oracle.OracleLM(w.lm), oracle.OracleLM(lm2)], alphas,
+                       oracle.OracleTrie(w.V, w.blank, w.phrases), w.logits, S, B, k, w.beta, w.blank, 1,
+                       [[w.V] * H, [w.V] * H], [0] * H, sc0, forced_tokens=out["tokens"].cpu().numpy(),
+                       forced_parents=out["parents"].cpu().numpy(), tol=TIE_TOL, threads=threads())
+    bad = np.nonzero(r["mismatch_at"] >= 0)[0]
+    assert bad.size == 0, f"streams {bad[:5]} diverge at frames {r['mismatch_at'][bad[:5]]}"
+    assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
+    assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
+    fin = np.isfinite(r["hyp_score"])
+    assert np.array_equal(np.isfinite(sc.cpu().numpy()), fin)
+    err = np.abs(sc.cpu().numpy()[fin] - r["hyp_score"][fin]).max()
+    assert err <= T * SCORE_TOL, f"final beam score error {err}"
+    print(f"C5 + keyword LM: {H} hypotheses x {T} frames agree; near ties {int(r['near_ties'].sum())}")

@@ -17,6 +17,7 @@ from .gen import (  # noqa: F401
     make_phrases,
     make_logits,
     make_projection,
+    make_keyword_lm,
     to_bf16_bits,
     load_workload,
     tiny_random_lm,

@@ -421,6 +421,34 @@ def load_workload(cfg: int, T: int | None = None, S: int | None = None,
                               cutoffs=list(c["cutoffs"]), n_phrases=c["n_phr"]))
 
 
+def make_keyword_lm(cfg: int = 5, n_sent: int = 300_000, N: int = 4, len_range=(3, 12)) -> LMArrays:
+    """A second LM over the vocabulary of workload ``cfg``, of the shape of the
+    keyword LM of Sec. IV-A (an n = 4 model of synthesized text around the
+    user's terms): short Zipf carrier sentences, each with one phrase of the
+    workload's boost list inserted at a uniform position, estimated with
+    interpolated KN and no cutoffs.  Synthetic tokens only."""
+    c = CONFIGS[cfg]
+    V = c["V"]
+    w = load_workload(cfg, T=1, S=1, with_logits=False)
+    phr = w.phrases.as_lists()
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([2609, 14991, int(cfg), 6])))
+    toks, offs = make_corpus(rng, n_sent, V, c["zipf"], len_range=len_range)
+    pick = rng.integers(0, len(phr), size=n_sent)
+    lens = np.diff(offs)
+    pos = (rng.random(n_sent) * (lens + 1)).astype(np.int64)
+    out_lens = lens + np.array([len(phr[i]) for i in pick], dtype=np.int64)
+    out_offs = np.zeros(n_sent + 1, dtype=np.int64)
+    np.cumsum(out_lens, out=out_offs[1:])
+    out = np.empty(int(out_offs[-1]), dtype=np.int32)
+    for i in range(n_sent):
+        a, b, o, q = int(offs[i]), int(offs[i + 1]), int(out_offs[i]), int(pos[i])
+        p = phr[pick[i]]
+        out[o:o + q] = toks[a:a + q]
+        out[o + q:o + q + len(p)] = p
+        out[o + q + len(p):int(out_offs[i + 1])] = toks[a + q:b]
+    return estimate_kn(out, out_offs, V, N, tuple([1] * N))
+
+
 # --------------------------------------------------------------------------
 # tiny random cases for property tests
 # --------------------------------------------------------------------------
