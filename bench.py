@@ -40,6 +40,7 @@ def log(msg):
 KERNEL_SOURCES = ("paper_2609_14991_amd/csrc/fusion_kernels.hip", "paper_2609_14991_amd/csrc/fusion_internal.h",
                   "paper_2609_14991_amd/csrc/ngram_tables.cpp", "paper_2609_14991_amd/csrc/boost_trie.cpp")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fusion_kernel_c5_hbm_traffic.md")
+TRAFFIC_FILE_TWO_LMS = os.path.join(ROOT, "profiles", "fusion_kernel_c5_two_lms_hbm_traffic.md")
 
 
 def kernel_sources_digest():
@@ -50,11 +51,12 @@ def kernel_sources_digest():
     return h.hexdigest()[:16]
 
 
-def recorded_traffic(workload):
+def recorded_traffic(workload, path=None):
     """(bytes per launch, source digest) from the committed PMC summary, or None."""
-    if not os.path.exists(TRAFFIC_FILE):
+    path = TRAFFIC_FILE if path is None else path
+    if not os.path.exists(path):
         return None
-    txt = open(TRAFFIC_FILE).read()
+    txt = open(path).read()
     fields = dict(re.findall(r"^- (\w+): `([^`]*)`", txt, re.M))
     if fields.get("workload") != workload or "traffic_bytes_per_launch" not in fields:
         return None
@@ -299,6 +301,12 @@ def main():
                          "frac": ach2 / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg2,
                          "bytes_per_hyp_step": alg2 / max(steps2, 1)},
         }
+        rec2 = recorded_traffic(w.name + "+keyword4", TRAFFIC_FILE_TWO_LMS)
+        ok2 = rec2 is not None and rec2[1] == kernel_sources_digest()
+        out["two_lms"]["roofline"]["traffic"] = rec2[0] if ok2 else None
+        out["two_lms"]["roofline"]["traffic_note"] = (
+            "HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)" if ok2
+            else "no PMC record for these kernel sources")
         log(f"two LMs: {k2:.3f} ms kernel, {alg2 / max(steps2, 1):.0f} B/hyp-step, {ach2:.1f} GB/s")
         del lm2
 
