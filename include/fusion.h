@@ -180,7 +180,9 @@ int fusion_step(const NgramTables *lm, const BoostTrie *trie, const float *logit
  *                and a dense row, phrase rows, outputs) and the number of
  *                hypothesis-steps processed
  * States carry across calls, so a stream can be decoded chunk by chunk with
- * the same result as one call over all frames.
+ * the same result as one call over all frames.  T == 0 checks the scalar
+ * arguments and handles and returns FUSION_OK without reading or writing any
+ * buffer (logits and outputs may then be NULL).
  */
 int fusion_run(const NgramTables *lm, const BoostTrie *trie, const float *logits, int32_t T,
                int32_t S, int32_t B, int32_t V, int32_t k, float lambda, float beta,

@@ -1255,7 +1255,8 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
 }
 
 int check_common(const NgramTables *const *lms, const float *alphas, int32_t n_lm, const BoostTrie *trie,
-                 const float *logits, int32_t V, int32_t k, int32_t blank_id, int32_t blank_mode, float beta) {
+                 const float *logits, int32_t V, int32_t k, int32_t blank_id, int32_t blank_mode, float beta,
+                 bool need_logits = true) {
   if (n_lm < 1 || n_lm > FUSION_MAX_LMS) return set_error(FUSION_E_ARG, "n_lm out of range");
   if (!lms || !alphas) return set_error(FUSION_E_ARG, "NULL LM list or weights");
   for (int i = 0; i < n_lm; ++i) {
@@ -1264,7 +1265,7 @@ int check_common(const NgramTables *const *lms, const float *alphas, int32_t n_l
     if (blank_id != lms[i]->dev.blank) return set_error(FUSION_E_ARG, "blank_id does not match the n-gram tables");
     if (!std::isfinite(alphas[i])) return set_error(FUSION_E_ARG, "non-finite fusion weight");
   }
-  if (!logits) return set_error(FUSION_E_ARG, "NULL logits");
+  if (need_logits && !logits) return set_error(FUSION_E_ARG, "NULL logits");
   if (trie && (trie->dev.V != V || trie->dev.blank != blank_id))
     return set_error(FUSION_E_ARG, "phrase tree built for another vocabulary or blank");
   if (k < 1 || k > FUSION_MAX_K || k > V) return set_error(FUSION_E_ARG, "k out of range");
@@ -1321,15 +1322,15 @@ int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, c
              const float *logits, int32_t T, int32_t S, int32_t B, int32_t V, int32_t k, float beta,
              int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state, double *hyp_score,
              int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, hipStream_t stream) {
-  int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta);
+  int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta, T != 0);
   if (rc != FUSION_OK) return rc;
   if (T < 0 || S < 1 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
   if ((int64_t)S * B > (1 << 24)) return set_error(FUSION_E_ARG, "too many hypotheses");
   if (B == 1 && k != 1) return set_error(FUSION_E_ARG, "greedy decoding (B == 1) needs k == 1");
   if (B > 1 && blank_mode != FUSION_BLANK_COMPETE) return set_error(FUSION_E_ARG, "beam decoding needs FUSION_BLANK_COMPETE");
+  if (T == 0) return FUSION_OK;  // nothing to decode: no buffer is read or written
   if (!lm_state || !tokens || (trie && !boost_state)) return set_error(FUSION_E_ARG, "NULL state or output buffer");
   if (B > 1 && (!hyp_score || !parents)) return set_error(FUSION_E_ARG, "beam decoding needs hyp_score and parents");
-  if (T == 0) return FUSION_OK;
   Params p = make_params(lms, alphas, n_lm, trie);
   p.logits = logits;
   p.lm_state = lm_state;
