@@ -217,6 +217,26 @@ int fusion_run_lms(const NgramTables *const *lms, const float *alphas, int32_t n
                    int32_t *parents, float *fused, int64_t *traffic, hipStream_t stream);
 
 /*
+ * fusion_end_scores - end-of-stream scoring: the LM terms of Eq. (1) for the
+ * end-of-sentence token </s>, added when a stream ends so that its hypotheses
+ * are compared as complete sentences.
+ *   lms, alphas, n_lm  as in fusion_run_lms (every LM must contain </s>:
+ *                      FUSION_E_UNSUPPORTED otherwise)
+ *   lm_state     device [n_lm, H] final LM state ids (as fusion_run_lms leaves them)
+ *   hyp_score    device [H] fp64 or NULL: in/out, hyp_score[h] += t_1, += t_2, ...
+ *                with t_i = fl32(alphas[i] * lm_i(</s> | state)) in LM order;
+ *                -inf (dead) stays -inf
+ *   end_term     device [H] fp64 or NULL: out, (0 + t_1) + t_2 ...
+ * lm_i(</s> | state) is the backoff recursion of fusion_step in fp32.  At
+ * least one of hyp_score / end_term must be given.  A state that is blank,
+ * </s> or out of range adds nothing for that LM and sets
+ * FUSION_STATUS_BAD_LM_STATE (fusion_device_status).  Only enqueues work.
+ */
+int fusion_end_scores(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
+                      const int32_t *lm_state, int32_t H, double *hyp_score, double *end_term,
+                      hipStream_t stream);
+
+/*
  * joint_project - output projection of the Transducer joint network (the
  * network whose log-softmax is the acoustic term of Eq. (1), Sec. III-C),
  * for M hypothesis-frames at once, on the matrix cores:

@@ -91,6 +91,8 @@ def lib():
         L.or_step_lms.argtypes = [ctypes.POINTER(vp), f32p, c_int, vp, f32p, i32p, i32p, c_int,
                                   c_int, c_float, c_int, c_int, c_int, f32p, f64p, f64p, i32p,
                                   f64p, i32p, i32p]
+        L.or_end_scores.restype = c_int
+        L.or_end_scores.argtypes = [ctypes.POINTER(vp), f32p, c_int, i32p, c_int, f64p, f64p]
         L.or_run_lms.restype = c_int
         L.or_run_lms.argtypes = [ctypes.POINTER(vp), f32p, c_int, vp, f32p, c_int, c_int, c_int,
                                  c_int, c_int, c_float, c_int, c_int, i32p, i32p, f64p, i32p, i32p,
@@ -365,3 +367,19 @@ def run_lms(lms, alphas, trie: OracleTrie | None, logits, S, B, k, beta, blank, 
         raise OracleError(_err())
     return dict(tokens=tok, parents=par, sel_score=sel, lm_state=lo, boost_state=bo,
                 hyp_score=so if B > 1 else None, near_ties=near[:S], mismatch_at=mis[:S])
+
+
+def end_scores(lms, alphas, lm_states, hyp_score=None):
+    """End of stream: per hypothesis the weighted LM terms of </s> (each LM's
+    fp32 backoff value, fp32 product), added in LM order to ``hyp_score`` (a
+    new array; None: zeros).  Returns (new scores, end terms)."""
+    hs, al, n = _lm_list(lms, alphas)
+    ls = np.ascontiguousarray(np.asarray(lm_states).reshape(n, -1), dtype=np.int32)
+    H = ls.shape[1]
+    sc = np.zeros(H, np.float64) if hyp_score is None else np.array(hyp_score, dtype=np.float64)
+    term = np.empty(H, np.float64)
+    rc = lib().or_end_scores(hs, _p(al, ctypes.c_float), n, _p(ls, ctypes.c_int32), H,
+                             _p(sc, ctypes.c_double), _p(term, ctypes.c_double))
+    if rc != 0:
+        raise OracleError(_err())
+    return sc, term

@@ -1028,3 +1028,34 @@ int or_run(const OrLM *lm, const OrTrie *tr, const float *logits, int T, int S, 
                     boost_state, hyp_score, tokens, parents, sel_score, lm_out, boost_out, score_out,
                     forced_tok, forced_par, tol, near_ties, mismatch_at, n_threads);
 }
+
+/* ------------------------------------------------------------------------ */
+/* end of stream: the LM terms of </s>                                        */
+/* ------------------------------------------------------------------------ */
+/* For each hypothesis h and LM i (in order): t_i = fl32(lam_i * lm_i(</s> |
+   state)) with lm_i the fp32 backoff recursion; hyp_score[h] += t_i in fp64
+   (in/out, or NULL), end_term[h] = (0 + t_1) + t_2 ... (or NULL).  lm_state is
+   [n_lm][H].  A state that is blank or </s> is an error. */
+int or_end_scores(const OrLM *const *lms, const float *lams, int n_lm, const int32_t *lm_state, int H,
+                  double *hyp_score, double *end_term) {
+  g_err[0] = 0;
+  if (n_lm < 1 || n_lm > OR_MAXLM || !lms || !lams || H < 0) return fail(OR_EARG, "bad end arguments");
+  for (int i = 0; i < n_lm; ++i)
+    if (!lms[i]) return fail(OR_EARG, "bad end arguments");
+  int32_t t[OR_MAXN + 2];
+  for (int h = 0; h < H; ++h) {
+    double term = 0.0;
+    for (int i = 0; i < n_lm; ++i) {
+      const OrLM *lm = lms[i];
+      int len = or_lm_state_tuple(lm, lm_state[(int64_t)i * H + h], t);
+      if (len < 0 || (len == 1 && (t[0] == lm->blank || t[0] == lm->V + 1)))
+        return fail(OR_EARG, "invalid LM state");
+      float v = or_lm_logp32(lm, t, len, lm->V + 1);
+      float a = lams[i] * v;
+      term = term + (double)a;
+      if (hyp_score) hyp_score[h] = hyp_score[h] + (double)a;
+    }
+    if (end_term) end_term[h] = term;
+  }
+  return OR_OK;
+}

@@ -34,7 +34,7 @@ FUSION_MAX_LMS = 2
 
 EXPORTS = ("ngram_load", "ngram_bos_state", "ngram_info", "ngram_free", "boost_build", "boost_info",
            "boost_free", "fusion_step", "fusion_run", "fusion_step_lms", "fusion_run_lms",
-           "joint_project", "fusion_last_error", "fusion_device_status")
+           "fusion_end_scores", "joint_project", "fusion_last_error", "fusion_device_status")
 
 
 class FusionError(RuntimeError):
@@ -82,6 +82,8 @@ def lib():
         L.fusion_run_lms.restype = ctypes.c_int
         L.fusion_run_lms.argtypes = [vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f32, i32, i32, vp,
                                      vp, vp, vp, vp, vp, vp, vp]
+        L.fusion_end_scores.restype = ctypes.c_int
+        L.fusion_end_scores.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp]
         L.joint_project.restype = ctypes.c_int
         L.joint_project.argtypes = [vp, vp, vp, i32, i32, i32, vp, vp]
         L.fusion_last_error.restype = ctypes.c_char_p
@@ -262,6 +264,14 @@ def fusion_run_lms(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, bla
                                 int(blank_mode), _ptr(lm_state), _ptr(boost_state), _ptr(hyp_score),
                                 _ptr(tokens), _ptr(parents), _ptr(fused), _ptr(traffic),
                                 _stream(stream)))
+
+
+def fusion_end_scores(lms, alphas, lm_state, H, hyp_score=None, end_term=None, stream=None):
+    """Same arguments as the C call; lm_state [n_lm, H] int32, hyp_score / end_term
+    [H] float64 CUDA tensors (either may be None, not both)."""
+    hs, al, n = _lm_arrays(lms, alphas)
+    _check(lib().fusion_end_scores(ctypes.cast(hs, ctypes.c_void_p), _ptr(al), n, _ptr(lm_state), int(H),
+                                   _ptr(hyp_score), _ptr(end_term), _stream(stream)))
 
 
 def joint_project(A, W, bias, M, N, K, out, stream=None):

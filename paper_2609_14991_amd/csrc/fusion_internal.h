@@ -32,6 +32,7 @@ struct LMDevice {
   const float *dense = nullptr;        // [(V+2) * V]  level-1 row of every one-token context
   const int32_t *rec_dense = nullptr;  // [(V+2) * V * rec_stride]  record of the state after (w, y)
   const int32_t *cnt1 = nullptr;       // [V+2]        explicit bigram successors with y < V
+  const float *eos1 = nullptr;         // [V+2]        level-1 value of </s>: p*(w </s>), else uni(</s>) + bo(w)
   const int32_t *rec = nullptr;        // [(n_states - (V+2)) * rec_stride] state records
   const int2 *arcs = nullptr;          // (token, logp bits) of the arcs of levels 2..N-1, level by level
   int64_t arc_base[FUSION_MAX_ORDER] = {};  // first arc of level L (arcs of order L+1 n-grams)
@@ -95,4 +96,6 @@ namespace fusion {
 // thread-local error text behind fusion_last_error()
 int set_error(int code, const std::string &msg);
 int hip_error(hipError_t e, const char *what);
+// status bits of the end-of-stream kernel, taken and cleared (end_scores.hip)
+int end_status_take(int32_t *bits);
 }  // namespace fusion

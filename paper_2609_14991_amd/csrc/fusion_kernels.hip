@@ -1369,7 +1369,10 @@ extern "C" int fusion_device_status(hipStream_t stream, int32_t *code) {
   int zero = 0;
   e = hipMemcpyToSymbol(HIP_SYMBOL(g_status), &zero, sizeof(int), 0, hipMemcpyHostToDevice);
   if (e != hipSuccess) return hip_error(e, "hipMemcpyToSymbol");
-  *code = v;
+  int32_t end_bits = 0;
+  const int rc = end_status_take(&end_bits);
+  if (rc != FUSION_OK) return rc;
+  *code = v | end_bits;
   return FUSION_OK;
 }
 

@@ -238,6 +238,17 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
       }
     }
   });
+  // ---- level-1 value of </s> per one-token context (the dense rows hold y < V) ----
+  std::vector<float> eos1(V + 2, 0.0f);
+  if (d.eos_ok) {
+    for (int64_t w = 0; w < V + 2; ++w) {
+      eos1[w] = uni_lp[EOS] + uni_bo[w];
+      const int64_t u = uni_row[w];
+      if (u < 0) continue;
+      const int64_t beg = arc_beg[1][u], n = arc_cnt[1][u];
+      if (n > 0 && tok_of(2, beg + n - 1, 1) == EOS) eos1[w] = lp_of(2, beg + n - 1);  // </s> sorts last
+    }
+  }
   // ---- arcs of levels 2..N-1 (order L+1 n-grams), one array level by level -----
   int64_t n_arcs = 0;
   for (int L = 2; L <= N - 1; ++L) {
@@ -304,6 +315,7 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
   if (rc == FUSION_OK) rc = up.put(dense, &d.dense);
   if (rc == FUSION_OK) rc = up.put(rec_dense, &d.rec_dense);
   if (rc == FUSION_OK) rc = up.put(cnt1, &d.cnt1);
+  if (rc == FUSION_OK) rc = up.put(eos1, &d.eos1);
   if (rc == FUSION_OK) rc = up.put(rec, &d.rec);
   if (rc == FUSION_OK) rc = up.put(arcs, &d.arcs);
   if (rc == FUSION_OK) rc = up.put(top_next, &d.top_next);

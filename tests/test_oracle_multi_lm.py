@@ -153,3 +153,46 @@ def test_two_lm_exhaustive_beam_keeps_every_path():
                 phh.append(y)
         brute.append(tot)
     assert np.allclose(np.sort(r["hyp_score"])[::-1], sorted(brute, reverse=True), atol=1e-9, rtol=0)
+
+
+def test_end_scores_hand_values():
+    """End of stream on the hand example LM: the </s> term of a state is
+    alpha ln p(</s> | state) with the hand-worked probabilities (context (3):
+    0.1; context (1 2): bo(1 2) * P(</s>|2) = 0.625 * 0.1), and with two LMs the
+    terms add in order onto the running score (dead slots stay -inf)."""
+    g, lm = hand_lm()
+    olm = oracle.OracleLM(lm)
+    ids = {tuple(t): sid for t, sid in g["state_ids"]["tuples"]}
+    s3, s12 = 3, ids[(1, 2)]
+    sc, term = oracle.end_scores([olm], [0.5], [[s3, s12]], [-1.0, 2.0])
+    assert term[0] == pytest.approx(0.5 * math.log(0.1), rel=1e-6)
+    assert term[1] == pytest.approx(0.5 * math.log(0.625 * 0.1), rel=1e-6)
+    assert np.array_equal(sc, np.array([-1.0, 2.0]) + term)
+    sc2, term2 = oracle.end_scores([olm, olm], [0.5, 0.25], [[s3, s3, s12], [s12, s3, s3]],
+                                   [0.0, -np.inf, 1.0])
+    want0 = 0.5 * math.log(0.1) + 0.25 * math.log(0.0625)
+    assert term2[0] == pytest.approx(want0, rel=1e-6)
+    assert sc2[1] == -np.inf
+    assert sc2[2] == pytest.approx(1.0 + 0.5 * math.log(0.0625) + 0.25 * math.log(0.1), rel=1e-6)
+    with pytest.raises(oracle.OracleError):
+        oracle.end_scores([olm], [0.5], [[0]])  # the blank state
+
+
+def test_end_scores_complete_the_sentence_probability():
+    """Summed over a token path, the LM terms of every step plus the </s> term
+    give ln P(<s> path </s>) (alpha = 1, beta = 0, logits 0): the chain rule of
+    the LM, checked against the product of hand-worked conditionals."""
+    g, lm = hand_lm()
+    olm = oracle.OracleLM(lm)
+    # <s> 1 2 3 </s>: P(1|<s>) P(2|<s> 1) P(3|1 2) P(</s>|2 3)
+    p = 0.5 * 0.6 * 0.5 * (1.0 * 0.1)  # (2 3) absent: bo = 1, (3 </s>) absent: bo(3) = 1, P(</s>) = 0.1
+    V = g["V"]
+    x = np.zeros((1, V), np.float32)
+    ls, tot = [g["BOS"]], 0.0
+    lse = math.log(V)  # log-softmax of zero logits
+    for y in g["path"]["tokens"]:
+        r = oracle.step_lms([olm], [1.0], None, x, [ls], [0], 0.0, 0, V, 1)
+        tot += r["fused"][0, y] + lse
+        ls = [int(r["next_lm"][0, 0, list(r["tokens"][0]).index(y)])]
+    _, term = oracle.end_scores([olm], [1.0], [ls])
+    assert tot + term[0] == pytest.approx(math.log(p), rel=1e-6)

@@ -163,3 +163,77 @@ def test_two_lms_above_4096_tokens_are_unsupported():
     with pytest.raises(F.FusionError) as e:
         F.step_lms(lms, [0.5, 0.5], None, x, ls, None, 0.0, 0, 1, F.FUSION_BLANK_COMPETE)
     assert e.value.code == F.FUSION_E_UNSUPPORTED
+
+
+def test_end_scores_random_states():
+    """End-of-stream </s> terms at random states of every order, one and two
+    LMs: the GPU adds exactly what the oracle adds (same fp32 recursion and
+    product, same fp64 additions), dead slots stay -inf."""
+    rng = np.random.default_rng(31)
+    V, H = 1000, 300
+    lms = [tiny_random_lm(rng, V, 5, n_sent=4000), tiny_random_lm(rng, V, 3, n_sent=2000)]
+    glms = [F.ngram_load_arrays(m) for m in lms]
+    olms = [oracle.OracleLM(m) for m in lms]
+    states = np.stack([random_states(m, H, rng) for m in lms])
+    sc0 = rng.standard_normal(H) * 10
+    sc0[::7] = -np.inf
+    for n, alphas in [(1, [0.5]), (2, [0.5, 0.3])]:
+        sc = torch.from_numpy(sc0.copy()).to(dev())
+        term = torch.empty(H, dtype=torch.float64, device=dev())
+        F.fusion_end_scores(glms[:n], alphas, torch.from_numpy(states[:n].copy()).to(dev()), H, sc, term)
+        torch.cuda.synchronize()
+        assert F.fusion_device_status() == 0
+        want_sc, want_term = oracle.end_scores(olms[:n], alphas, states[:n], sc0)
+        assert np.array_equal(term.cpu().numpy(), want_term)
+        assert np.array_equal(sc.cpu().numpy(), want_sc)
+
+
+def test_end_scores_after_a_beam_run():
+    """A 30-frame two-LM beam, then the end-of-stream terms on its final
+    states: the completed scores equal the oracle's completion of its own
+    replay (within the beam's score tolerance) and every slot's ranking by
+    completed score is the oracle's."""
+    rng = np.random.default_rng(33)
+    V, S, B, k, T = 500, 8, 4, 4, 30
+    lms = [tiny_random_lm(rng, V, 4, n_sent=3000), tiny_random_lm(rng, V, 3, n_sent=2000)]
+    ph = tiny_random_phrases(rng, V, n=30, max_len=4, alphabet=30, with_completion=True)
+    glms = [F.ngram_load_arrays(m) for m in lms]
+    gtr = F.boost_build_phrases(V, 0, ph)
+    H = S * B
+    x = (rng.standard_normal((T, H, V)) * 2).astype(np.float32)
+    x[:, :, 0] += 2
+    alphas = [0.5, 0.25]
+    ls = torch.full((2, H), V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev())
+    sc0 = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)
+    sc = torch.from_numpy(sc0.copy()).to(dev())
+    out = F.run_lms(glms, alphas, gtr, torch.from_numpy(x).to(dev()), S, B, k, 0.5, 0, F.FUSION_BLANK_COMPETE,
+                    ls, bs, sc)
+    F.fusion_end_scores(glms, alphas, ls, H, sc)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    olms = [oracle.OracleLM(m) for m in lms]
+    r = oracle.run_lms(olms, alphas, oracle.OracleTrie(V, 0, ph), x, S, B, k, 0.5, 0, 1, [[V] * H, [V] * H],
+                       [0] * H, sc0, forced_tokens=out["tokens"].cpu().numpy(),
+                       forced_parents=out["parents"].cpu().numpy(), tol=TIE_TOL, threads=8)
+    assert (r["mismatch_at"] < 0).all()
+    want, _ = oracle.end_scores(olms, alphas, r["lm_state"], r["hyp_score"])
+    got = sc.cpu().numpy()
+    assert np.abs(got - want).max() <= T * SCORE_TOL
+    for s in range(S):
+        assert np.array_equal(np.argsort(-got[s * B:(s + 1) * B], kind="stable"),
+                              np.argsort(-want[s * B:(s + 1) * B], kind="stable"))
+
+
+def test_end_scores_flag_invalid_states():
+    rng = np.random.default_rng(35)
+    V = 300
+    glm = F.ngram_load_arrays(tiny_random_lm(rng, V, 3, n_sent=500))
+    states = torch.tensor([[V, 0, V + 1, 5]], dtype=torch.int32, device=dev())  # <s>, blank, </s>, token 5
+    term = torch.zeros(4, dtype=torch.float64, device=dev())
+    F.fusion_end_scores([glm], [1.0], states, 4, None, term)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == F.FUSION_STATUS_BAD_LM_STATE
+    t = term.cpu().numpy()
+    assert t[1] == 0.0 and t[2] == 0.0 and t[0] < 0 and t[3] < 0
+    assert F.fusion_device_status() == 0  # cleared by the read
