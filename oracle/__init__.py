@@ -96,7 +96,8 @@ def lib():
         L.or_run_lms.restype = c_int
         L.or_run_lms.argtypes = [ctypes.POINTER(vp), f32p, c_int, vp, f32p, c_int, c_int, c_int,
                                  c_int, c_int, c_float, c_int, c_int, i32p, i32p, f64p, i32p, i32p,
-                                 f64p, i32p, i32p, f64p, i32p, i32p, c_double, i64p, i64p, c_int]
+                                 f64p, i32p, i32p, f64p, i32p, i32p, c_double, i64p, i64p, c_int,
+                                 c_int]
         _lib = L
     return _lib
 
@@ -331,9 +332,11 @@ def step_lms(lms, alphas, trie: OracleTrie | None, logits, lm_states, boost_stat
 
 def run_lms(lms, alphas, trie: OracleTrie | None, logits, S, B, k, beta, blank, mode, lm_states,
             boost_state, hyp_score=None, forced_tokens=None, forced_parents=None, tol=1e-4,
-            threads=1):
+            threads=1, recombine=False):
     """``run`` with several LMs: ``lm_states`` is [n_lm, S*B] and the final LM
-    states come back as [n_lm, S*B]."""
+    states come back as [n_lm, S*B].  ``recombine`` (beam): candidates reaching
+    the same token history merge into the first of them in candidate order,
+    with the log-sum of their scores."""
     hs_, al, n = _lm_list(lms, alphas)
     x = np.ascontiguousarray(logits, dtype=np.float32)
     T, H, V = x.shape
@@ -362,7 +365,7 @@ def run_lms(lms, alphas, trie: OracleTrie | None, logits, S, B, k, beta, blank, 
                           _p(sel, ctypes.c_double), _p(lo, ctypes.c_int32), _p(bo, ctypes.c_int32),
                           _p(so, ctypes.c_double), _p(ft, ctypes.c_int32), _p(fp, ctypes.c_int32),
                           float(tol), _p(near, ctypes.c_int64), _p(mis, ctypes.c_int64),
-                          int(threads))
+                          int(threads), int(bool(recombine)))
     if rc != 0:
         raise OracleError(_err())
     return dict(tokens=tok, parents=par, sel_score=sel, lm_state=lo, boost_state=bo,

@@ -500,6 +500,7 @@ typedef struct {
   const OrTrie *tr;
   int V, blank, k, mode;
   float beta;
+  int recombine; /* beam: merge candidates that reach the same history */
 } Ctx;
 
 /* Histories: the context of LM i is the last <= N_i-1 tokens of its history
@@ -727,6 +728,33 @@ static void hyp_push(Hyp *h, int n_lm, int32_t y) {
   h->ph_hist[h->ph_len++] = y;
 }
 
+/* do hypotheses pa + ya and pb + yb (blank appends nothing) hold the same
+   history: the same LM histories (initial tuple and emitted tokens) for every
+   LM and the same phrase history?  Compared token by token. */
+static int same_history_after(const Hyp *pa, int32_t ya, const Hyp *pb, int32_t yb, int blank, int n_lm) {
+  const int ea = ya != blank, eb = yb != blank;
+  if (pa->ph_len + ea != pb->ph_len + eb) return 0;
+  for (int i = 0; i < n_lm; ++i)
+    if (pa->lm_len[i] + ea != pb->lm_len[i] + eb) return 0;
+  for (int i = 0; i <= n_lm; ++i) {
+    const int32_t *ha = i < n_lm ? pa->lm_hist[i] : pa->ph_hist;
+    const int32_t *hb = i < n_lm ? pb->lm_hist[i] : pb->ph_hist;
+    const int la = i < n_lm ? pa->lm_len[i] : pa->ph_len;
+    const int lb = i < n_lm ? pb->lm_len[i] : pb->ph_len;
+    for (int q = 0; q < la + ea; ++q) {
+      const int32_t va = q < la ? ha[q] : ya, vb = q < lb ? hb[q] : yb;
+      if (va != vb) return 0;
+    }
+  }
+  return 1;
+}
+
+/* log(exp(a) + exp(b)) in fp64 */
+static double log_add(double a, double b) {
+  const double m = a > b ? a : b, d = a > b ? b - a : a - b;
+  return m + log1p(exp(d));
+}
+
 static void hyp_copy(Hyp *d, const Hyp *p, int n_lm) {
   for (int i = 0; i < n_lm; ++i) {
     memcpy(d->lm_hist[i], p->lm_hist[i], (size_t)p->lm_len[i] * sizeof(int32_t));
@@ -817,6 +845,20 @@ static void *run_streams(void *arg) {
         if (J->sel_score) J->sel_score[(int64_t)t * H + h] = cand[0].score;
         if (y != c->blank) hyp_push(&hy[0], c->n_lm, y);
         continue;
+      }
+      /* recombination: candidates that reach the same history merge into the
+         first of them in candidate order (parent asc, rank asc); its score is
+         the log-sum of theirs, folded in that order */
+      if (c->recombine) {
+        int nr = 0;
+        for (int q = 0; q < nc; ++q) {
+          int r = -1;
+          for (int u = 0; u < nr && r < 0; ++u)
+            if (same_history_after(&hy[cand[u].b], cand[u].y, &hy[cand[q].b], cand[q].y, c->blank, c->n_lm)) r = u;
+          if (r < 0) cand[nr++] = cand[q];
+          else cand[r].score = log_add(cand[r].score, cand[q].score);
+        }
+        nc = nr;
       }
       /* beam: order candidates (score desc, parent asc, rank asc), keep B */
       for (int i = 1; i < nc; ++i) {
@@ -945,7 +987,7 @@ int or_run_lms(const OrLM *const *lms, const float *lams, int n_lm, const OrTrie
                const double *hyp_score, int32_t *tokens, int32_t *parents, double *sel_score,
                int32_t *lm_out, int32_t *boost_out, double *score_out, const int32_t *forced_tok,
                const int32_t *forced_par, double tol, int64_t *near_ties, int64_t *mismatch_at,
-               int n_threads) {
+               int n_threads, int recombine) {
   g_err[0] = 0;
   if (n_lm < 1 || n_lm > OR_MAXLM || !lms || !lams || T < 0 || S < 0 || B < 1 || B > 64 || k < 1 ||
       k > V || (B == 1 && k != 1) || (mode == 0 && k != 1) || (B > 1 && (!parents || !hyp_score)))
@@ -965,6 +1007,7 @@ int or_run_lms(const OrLM *const *lms, const float *lams, int n_lm, const OrTrie
   c.k = k;
   c.mode = mode;
   c.beta = beta;
+  c.recombine = recombine != 0 && B > 1;
   if (n_threads < 1) n_threads = 1;
   if (n_threads > S) n_threads = S > 0 ? S : 1;
   for (int s = 0; s < S; ++s) {
@@ -1026,7 +1069,7 @@ int or_run(const OrLM *lm, const OrTrie *tr, const float *logits, int T, int S, 
            int64_t *mismatch_at, int n_threads) {
   return or_run_lms(&lm, &lam, 1, tr, logits, T, S, B, V, k, beta, blank, mode, lm_state,
                     boost_state, hyp_score, tokens, parents, sel_score, lm_out, boost_out, score_out,
-                    forced_tok, forced_par, tol, near_ties, mismatch_at, n_threads);
+                    forced_tok, forced_par, tol, near_ties, mismatch_at, n_threads, 0);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -196,3 +196,41 @@ def test_end_scores_complete_the_sentence_probability():
         ls = [int(r["next_lm"][0, 0, list(r["tokens"][0]).index(y)])]
     _, term = oracle.end_scores([olm], [1.0], [ls])
     assert tot + term[0] == pytest.approx(math.log(p), rel=1e-6)
+
+
+@pytest.mark.parametrize("n_lm", [1, 2])
+def test_recombining_beam_is_the_forward_sum_per_history(n_lm):
+    """V = 3, T = 3, k = 3, B = 27 with recombination: no frame has more
+    distinct histories than slots (1, 3, 7, 15), so the beam is exact and each
+    surviving slot's score is the log-sum, over every alignment (token path
+    with blanks) that emits its history, of the path's score; the path scores
+    come from the Python statement, each LM evaluated from its own history."""
+    V, T, B, k = 3, 3, 27, 3
+    rng = np.random.default_rng(14)
+    lms = [tiny_random_lm(rng, V, 3, n_sent=30), tiny_random_lm(rng, V, 2, n_sent=30)][:n_lm]
+    ph = Phrases(tokens=np.array([1, 2, 2, 1, 1], np.int32), offsets=np.array([0, 2, 5], np.int64))
+    xs = rng.standard_normal((T, 1, V)).astype(np.float32) * 2
+    x = np.repeat(xs, B, axis=1)
+    lams, beta = [0.5, 0.25][:n_lm], 0.5
+    r = oracle.run_lms([oracle.OracleLM(m) for m in lms], lams, oracle.OracleTrie(V, 0, ph), x, 1, B, k,
+                       beta, 0, 1, [[V] * B] * n_lm, [0] * B, recombine=True)
+    rlms, rtr = [ref.RefLM(m) for m in lms], ref.RefTrie(ph)
+    per_history = {}
+    for path in itertools.product(range(V), repeat=T):
+        hists, phh, tot = [[V] for _ in range(n_lm)], [], 0.0
+        for t, y in enumerate(path):
+            _, fused, _ = ref.score_row_lms(rlms, lams, rtr, xs[t, 0], hists, phh, beta, 0)
+            tot += fused[y]
+            if y != 0:
+                for hh in hists:
+                    hh.append(y)
+                phh.append(y)
+        per_history.setdefault(tuple(phh), []).append(tot)
+    want = sorted((float(np.logaddexp.reduce(v)) for v in per_history.values()), reverse=True)
+    got = np.sort(r["hyp_score"][np.isfinite(r["hyp_score"])])[::-1]
+    assert len(want) == 15 and got.size == 15
+    assert np.allclose(got, want, atol=1e-9, rtol=0)
+    # without recombination the same beam keeps 27 paths, not 15 histories
+    r0 = oracle.run_lms([oracle.OracleLM(m) for m in lms], lams, oracle.OracleTrie(V, 0, ph), x, 1, B, k,
+                        beta, 0, 1, [[V] * B] * n_lm, [0] * B)
+    assert np.isfinite(r0["hyp_score"]).sum() == 27
