@@ -267,7 +267,7 @@ def main():
             bs.copy_(bs0)
             sc.copy_(sc0)
             F.fusion_run_lms(lms2, alphas2, trie, x, T, S, B, V, k, w.beta, w.blank, mode, ls2, bs, sc,
-                             tokens, parents if B > 1 else None, None, traffic, stream.cuda_stream)
+                             tokens, parents if B > 1 else None, None, traffic, stream=stream.cuda_stream)
 
         traffic2 = torch.zeros(2, dtype=torch.int64, device=dev)
         run2(traffic2)
@@ -285,7 +285,7 @@ def main():
             sc.copy_(sc0)
             a.record(stream)
             F.fusion_run_lms(lms2, alphas2, trie, x, T, S, B, V, k, w.beta, w.blank, mode, ls2, bs, sc,
-                             tokens, parents if B > 1 else None, None, None, stream.cuda_stream)
+                             tokens, parents if B > 1 else None, None, None, stream=stream.cuda_stream)
             b.record(stream)
         torch.cuda.synchronize()
         k2 = float(np.mean([a.elapsed_time(b) for a, b in ev]))

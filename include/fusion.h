@@ -83,6 +83,9 @@ enum { FUSION_STATUS_BAD_LM_STATE = 1, FUSION_STATUS_BAD_BOOST_STATE = 2,
 #define FUSION_MAX_BEAM 32
 #define FUSION_MAX_LMS 2     /* LMs per fusion_step_lms / fusion_run_lms call (2 needs V <= 4096) */
 
+/* flags of fusion_run_lms */
+#define FUSION_RUN_RECOMBINE 1 /* beam: merge candidates that reach the same history */
+
 typedef struct NgramTables NgramTables; /* opaque, device resident, immutable after load */
 typedef struct BoostTrie BoostTrie;     /* opaque, device resident, immutable after build */
 
@@ -199,6 +202,12 @@ int fusion_run(const NgramTables *lm, const BoostTrie *trie, const float *logits
  *   lm_state     device [n_lm, H] state ids (LM i's state of hypothesis h at
  *                i * H + h); fusion_run_lms writes the final states back there
  *   next_lm      (step) device [n_lm, H, k]: LM i's state after each selection
+ *   flags        (run) 0 or FUSION_RUN_RECOMBINE: beam recombination.  Candidates
+ *                that reach the same history (the slot's initial states and the
+ *                tokens emitted since, compared as a 48-bit hash) merge into the
+ *                first of them in candidate order (parent asc, rank asc), whose
+ *                total becomes the log-sum of theirs (fp64, folded in that
+ *                order); the others leave the ranking.  Ignored for B == 1.
  * Every other argument is as in fusion_step / fusion_run (beta is the boost
  * weight).  Keys are fp32 with one rounding per operation, the LM terms added
  * in the order of lms: key = (...((x + a_1 lm_1) + a_2 lm_2)...) + beta boost.
@@ -214,7 +223,7 @@ int fusion_run_lms(const NgramTables *const *lms, const float *alphas, int32_t n
                    const BoostTrie *trie, const float *logits, int32_t T, int32_t S, int32_t B,
                    int32_t V, int32_t k, float beta, int32_t blank_id, int32_t blank_mode,
                    int32_t *lm_state, int32_t *boost_state, double *hyp_score, int32_t *tokens,
-                   int32_t *parents, float *fused, int64_t *traffic, hipStream_t stream);
+                   int32_t *parents, float *fused, int64_t *traffic, int32_t flags, hipStream_t stream);
 
 /*
  * fusion_end_scores - end-of-stream scoring: the LM terms of Eq. (1) for the

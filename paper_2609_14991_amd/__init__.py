@@ -31,6 +31,7 @@ FUSION_STATUS_BAD_LM_STATE = 1
 FUSION_STATUS_BAD_BOOST_STATE = 2
 
 FUSION_MAX_LMS = 2
+FUSION_RUN_RECOMBINE = 1
 
 EXPORTS = ("ngram_load", "ngram_bos_state", "ngram_info", "ngram_free", "boost_build", "boost_info",
            "boost_free", "fusion_step", "fusion_run", "fusion_step_lms", "fusion_run_lms",
@@ -81,7 +82,7 @@ def lib():
                                       vp, vp, vp, vp, vp]
         L.fusion_run_lms.restype = ctypes.c_int
         L.fusion_run_lms.argtypes = [vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f32, i32, i32, vp,
-                                     vp, vp, vp, vp, vp, vp, vp]
+                                     vp, vp, vp, vp, vp, vp, i32, vp]
         L.fusion_end_scores.restype = ctypes.c_int
         L.fusion_end_scores.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp]
         L.joint_project.restype = ctypes.c_int
@@ -255,14 +256,14 @@ def fusion_step_lms(lms, alphas, trie, logits, lm_state, boost_state, H, V, beta
 
 
 def fusion_run_lms(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
-                   boost_state, hyp_score, tokens, parents, fused=None, traffic=None, stream=None):
+                   boost_state, hyp_score, tokens, parents, fused=None, traffic=None, flags=0, stream=None):
     """Same arguments as the C call; lms and alphas are Python sequences,
     tensors are CUDA (HIP) tensors (lm_state [n_lm, S*B])."""
     hs, al, n = _lm_arrays(lms, alphas)
     _check(lib().fusion_run_lms(ctypes.cast(hs, ctypes.c_void_p), _ptr(al), n, _h(trie), _ptr(logits),
                                 int(T), int(S), int(B), int(V), int(k), float(beta), int(blank_id),
                                 int(blank_mode), _ptr(lm_state), _ptr(boost_state), _ptr(hyp_score),
-                                _ptr(tokens), _ptr(parents), _ptr(fused), _ptr(traffic),
+                                _ptr(tokens), _ptr(parents), _ptr(fused), _ptr(traffic), int(flags),
                                 _stream(stream)))
 
 
@@ -357,8 +358,9 @@ def step_lms(lms, alphas, trie, logits, lm_state, boost_state, beta, blank_id, k
 
 
 def run_lms(lms, alphas, trie, logits, S, B, k, beta, blank_id, blank_mode, lm_state, boost_state,
-            hyp_score=None, want_fused=False, traffic=None, stream=None):
-    """``run`` with several LMs: lm_state [n_lm, S*B] is updated in place."""
+            hyp_score=None, want_fused=False, traffic=None, recombine=False, stream=None):
+    """``run`` with several LMs: lm_state [n_lm, S*B] is updated in place;
+    ``recombine`` merges beam candidates that reach the same history."""
     import torch
 
     T, H, V = logits.shape
@@ -367,5 +369,6 @@ def run_lms(lms, alphas, trie, logits, S, B, k, beta, blank_id, blank_mode, lm_s
     parents = torch.empty((T, H), dtype=torch.int32, device=dev) if B > 1 else None
     fused = torch.zeros((T, H, V), dtype=torch.float32, device=dev) if want_fused else None
     fusion_run_lms(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
-                   boost_state, hyp_score, tokens, parents, fused, traffic, stream)
+                   boost_state, hyp_score, tokens, parents, fused, traffic,
+                   FUSION_RUN_RECOMBINE if recombine else 0, stream)
     return dict(tokens=tokens, parents=parents, fused=fused)

@@ -77,7 +77,7 @@ struct Params {
   int32_t *next_lm;
   int32_t *next_boost;
   unsigned long long *xchg;  // beam exchange [S][2][B][k] candidate records of four tagged words
-  int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, n_lm;
+  int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, n_lm, recombine, pad;
   float lam[FUSION_MAX_LMS], beta;
 };
 
@@ -87,6 +87,17 @@ __device__ __forceinline__ bool before(float ka, int ya, float kb, int yb) {
 __device__ __forceinline__ float as_float(int v) { return __int_as_float(v); }
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ __forceinline__ int rdl(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+// the splitmix64 finalizer: a 64-bit mix for the beam's history hashes
+__device__ __forceinline__ unsigned long long mix64(unsigned long long z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+// log(exp(a) + exp(b)) in fp64
+__device__ __forceinline__ double log_add(double a, double b) {
+  const double m = a > b ? a : b, d = a > b ? b - a : a - b;
+  return m + log1p(exp(d));
+}
 __device__ __forceinline__ unsigned long long umin64(unsigned long long a, unsigned long long b) {
   return a < b ? a : b;
 }
@@ -208,6 +219,7 @@ struct HypState {
   int qsrc, y, fl;  // phrase source, token; flags 1 alive, 2 invalid
   int cur_q;        // phrase state scored this frame
   double S;         // running beam score
+  unsigned long long hist;  // 48-bit hash of the history (initial states, emitted tokens): recombination
 };
 
 // first lane of LM i's record in the record word
@@ -246,6 +258,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   __shared__ int2 s_xb[NL > 1 ? FUSION_MAX_BEAM * FUSION_MAX_K : 1];
   __shared__ int s_xf[FUSION_MAX_BEAM * FUSION_MAX_K];
   __shared__ double s_tot[FUSION_MAX_BEAM * FUSION_MAX_K];
+  __shared__ unsigned long long s_hh[FUSION_MAX_BEAM * FUSION_MAX_K];  // history hash after each candidate
+  __shared__ double s_mt[FUSION_MAX_BEAM * FUSION_MAX_K];              // merged totals (recombination)
   __shared__ long long s_sbase[NL][kMaxLevels];  // state id of arc index i of level L < N-1: s_sbase[L] + i
   __shared__ int s_lbeg[NL][kMaxLevels];  // first arc of each level of the current state
   __shared__ int s_cfg[2];  // V, blank: re-read each frame so per-token masks stay inside the loop
@@ -326,6 +340,11 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     hs.fl = (alive ? 1 : 0) | ((ok_lm && ok_q) ? 0 : 2);
     hs.cur_q = q;
     hs.S = sc;
+    // the history starts at the slot's initial states
+    unsigned long long hh = mix64(0x243F6A8885A308D3ull ^ (unsigned long long)(unsigned)q);
+#pragma unroll
+    for (int i = 0; i < NL; ++i) hh = mix64(hh ^ ((unsigned long long)(unsigned)hs.lmsrc[i] << (8 * i + 1)));
+    hs.hist = hh & ((1ull << 48) - 1);
     if (alive && !(ok_lm && ok_q))
       atomicOr(&g_status, (ok_lm ? 0 : FUSION_STATUS_BAD_LM_STATE) | (ok_q ? 0 : FUSION_STATUS_BAD_BOOST_STATE));
   }
@@ -957,17 +976,19 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
       } else {
         // ---- beam: publish this hypothesis' candidates, meet the stream, rank all ----
-        // A candidate record is XW = 3 + NL 64-bit words, each carrying the frame
+        // A candidate record is XW = 4 + NL 64-bit words, each carrying the frame
         // tag in its top 16 bits over 48 bits of payload: the total score S_b +
         // fused (fp64), the first LM's and the phrase source, the token, the
-        // parent's c_1 (first LM) and flags, and for a second LM its source and
-        // the parent's c_1.  Words are written and read as relaxed agent-scope
+        // parent's c_1 (first LM) and flags, for a second LM its source and the
+        // parent's c_1, and (recombination only) the hash of the history the
+        // candidate reaches.  Words are written and read as relaxed agent-scope
         // atomics, so a reader that sees the current tag in all words holds the
         // whole record: polling the records is the rendezvous (no counter, no
         // fence).  Frames alternate between two buffers; a writer can be at most
         // one frame ahead of any reader of its stream, so it never overwrites a
         // buffer that is still being read.
-        constexpr int XW = 3 + NL;
+        constexpr int XW = 4 + NL;
+        const int nw = p.recombine ? XW : XW - 1;  // words written and polled
         unsigned long long *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * XW;
         const unsigned long long tag = (unsigned long long)((t + 1) & 0xFFFF) << 48;
         constexpr unsigned long long kPay = (1ull << 48) - 1;
@@ -982,9 +1003,14 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           w[3] = (unsigned long long)((hs.c1[0] + 1) & 0xFFFF) | ((unsigned long long)(hs.fl & 0xFF) << 16) | tag;
           if constexpr (NL > 1)
             w[4] = (unsigned long long)(unsigned)cl[1] | ((unsigned long long)((hs.c1[1] + 1) & 0xFFFF) << 32) | tag;
+          // the history after the candidate: blank emits nothing
+          const unsigned long long hist = hs.hist;
+          w[XW - 1] = ((!has || cy == blank) ? hist
+                                              : (mix64(hist ^ (0x632BE59BD9B4E019ull * (unsigned long long)(cy + 1))) & kPay)) |
+                      tag;
 #pragma unroll
           for (int q = 0; q < XW; ++q)
-            __hip_atomic_store(xs + (b * K + lane) * XW + q, w[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (q < nw) __hip_atomic_store(xs + (b * K + lane) * XW + q, w[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         // every workgroup of the stream ranks the same B*k candidates by (total
         // desc, parent asc, rank asc), i.e. candidate order breaks ties; slot b
@@ -1000,7 +1026,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           for (int spins = 0;; ++spins) {
             if (i < nc) {
 #pragma unroll
-              for (int q = 0; q < XW; ++q) w[q] = __hip_atomic_load(xs + i * XW + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              for (int q = 0; q < XW; ++q)
+                w[q] = q < nw ? __hip_atomic_load(xs + i * XW + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : tag;
               cur = true;
 #pragma unroll
               for (int q = 0; q < XW; ++q) cur = cur && (w[q] & ~kPay) == tag;
@@ -1021,6 +1048,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             s_xf[i] = (int)((w[3] >> 16) & 0xFF);
             if constexpr (NL > 1)
               s_xb[i] = make_int2((int)(unsigned)(w[4] & 0xFFFFFFFFull), (int)((w[4] >> 32) & 0xFFFF) - 1);
+            s_hh[i] = w[XW - 1] & kPay;
             s_tot[i] = valid ? __longlong_as_double((long long)((w[0] & kPay) | ((w[1] & 0xFFFF) << 48)))
                              : __longlong_as_double(0x7FF8000000000000ll);
           }
@@ -1028,6 +1056,43 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        if (p.recombine) {
+          // recombination: candidates that reach the same history (equal hash)
+          // merge into the first of them in candidate order, with the log-sum
+          // of their totals folded in that order; the others leave the ranking
+#pragma unroll 1
+          for (int i = lane; i < nc; i += 64) {
+            double m = __longlong_as_double(0x7FF8000000000000ll);
+            const double ti = s_tot[i];
+            if (ti == ti) {
+              const unsigned long long hi = s_hh[i];
+              int first = -1;
+              double acc = 0.0;
+#pragma unroll 1
+              for (int j = 0; j < nc; ++j) {
+                const double tj = s_tot[j];
+                if (tj == tj && s_hh[j] == hi) {
+                  if (first < 0) {
+                    first = j;
+                    acc = tj;
+                  } else {
+                    acc = log_add(acc, tj);
+                  }
+                }
+              }
+              if (first == i) m = acc;
+            }
+            s_mt[i] = m;
+          }
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+#pragma unroll 1
+          for (int i = lane; i < nc; i += 64) s_tot[i] = s_mt[i];
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        }
         int wi = -1;
         for (int i = lane; i < nc; i += 64) {
           const double ti = s_tot[i];
@@ -1063,6 +1128,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           hs.qsrc = a.z;
           hs.y = y;
           hs.fl = 1 | (s_xf[wi] & 2);
+          hs.hist = s_hh[wi];
           hs.S = s_tot[wi];
           p.tokens[o] = y;
           p.parents[o] = wi / K;
@@ -1223,8 +1289,8 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   int s_batch = (int)std::min<long>(p.S, resident / p.B);
   if (s_batch >= 8) s_batch -= s_batch % 8;
   if (s_batch < 1) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device at once");
-  // exchange records: 2 buffers x B x k candidates x (3 + n_lm) words per stream
-  const size_t xwords = (size_t)s_batch * 2 * p.B * p.k * (3 + p.n_lm);
+  // exchange records: 2 buffers x B x k candidates x (4 + n_lm) words per stream
+  const size_t xwords = (size_t)s_batch * 2 * p.B * p.k * (4 + p.n_lm);
   void *scratch = nullptr;
   e = hipMallocAsync(&scratch, xwords * sizeof(unsigned long long), stream);
   if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
@@ -1321,13 +1387,14 @@ int step_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, 
 int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, const BoostTrie *trie,
              const float *logits, int32_t T, int32_t S, int32_t B, int32_t V, int32_t k, float beta,
              int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state, double *hyp_score,
-             int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, hipStream_t stream) {
+             int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, int32_t flags, hipStream_t stream) {
   int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta, T != 0);
   if (rc != FUSION_OK) return rc;
   if (T < 0 || S < 1 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
   if ((int64_t)S * B > (1 << 24)) return set_error(FUSION_E_ARG, "too many hypotheses");
   if (B == 1 && k != 1) return set_error(FUSION_E_ARG, "greedy decoding (B == 1) needs k == 1");
   if (B > 1 && blank_mode != FUSION_BLANK_COMPETE) return set_error(FUSION_E_ARG, "beam decoding needs FUSION_BLANK_COMPETE");
+  if (flags & ~FUSION_RUN_RECOMBINE) return set_error(FUSION_E_ARG, "unknown flags");
   if (T == 0) return FUSION_OK;  // nothing to decode: no buffer is read or written
   if (!lm_state || !tokens || (trie && !boost_state)) return set_error(FUSION_E_ARG, "NULL state or output buffer");
   if (B > 1 && (!hyp_score || !parents)) return set_error(FUSION_E_ARG, "beam decoding needs hyp_score and parents");
@@ -1349,6 +1416,7 @@ int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, c
   p.mode = blank_mode;
   p.step_mode = 0;
   p.beta = beta;
+  p.recombine = (flags & FUSION_RUN_RECOMBINE) && B > 1;
   return launch(p, S * B, stream);
 }
 
@@ -1400,14 +1468,15 @@ extern "C" int fusion_run(const NgramTables *lm, const BoostTrie *trie, const fl
                           double *hyp_score, int32_t *tokens, int32_t *parents, float *fused,
                           int64_t *traffic, hipStream_t stream) {
   return run_impl(&lm, &lambda, 1, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
-                  boost_state, hyp_score, tokens, parents, fused, traffic, stream);
+                  boost_state, hyp_score, tokens, parents, fused, traffic, 0, stream);
 }
 
 extern "C" int fusion_run_lms(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
                               const BoostTrie *trie, const float *logits, int32_t T, int32_t S, int32_t B,
                               int32_t V, int32_t k, float beta, int32_t blank_id, int32_t blank_mode,
                               int32_t *lm_state, int32_t *boost_state, double *hyp_score, int32_t *tokens,
-                              int32_t *parents, float *fused, int64_t *traffic, hipStream_t stream) {
+                              int32_t *parents, float *fused, int64_t *traffic, int32_t flags,
+                              hipStream_t stream) {
   return run_impl(lms, alphas, n_lm, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
-                  boost_state, hyp_score, tokens, parents, fused, traffic, stream);
+                  boost_state, hyp_score, tokens, parents, fused, traffic, flags, stream);
 }

@@ -169,3 +169,30 @@ def test_c5_two_lms_full_beam():
     err = np.abs(sc.cpu().numpy()[fin] - r["hyp_score"][fin]).max()
     assert err <= T * SCORE_TOL, f"final beam score error {err}"
     print(f"C5 + keyword LM: {H} hypotheses x {T} frames agree; near ties {int(r['near_ties'].sum())}")
+
+
+def test_c5_recombining_beam():
+    """C5 with beam recombination (candidates reaching the same history merge,
+    log-summed): the oracle, comparing full histories, replays every decision
+    of the 64 x 4 beam over 300 frames."""
+    w = load_workload(5)
+    lm, trie, olm, otr = handles(w)
+    S, B, k, T = w.S, w.B, w.k, w.T
+    H = S * B
+    ls = torch.full((1, H), w.V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev())
+    sc0 = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)
+    sc = torch.from_numpy(sc0.copy()).to(dev())
+    out = F.run_lms([lm], [w.lam], trie, torch.from_numpy(w.logits).to(dev()), S, B, k, w.beta, w.blank,
+                    F.FUSION_BLANK_COMPETE, ls, bs, sc, recombine=True)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.run_lms([olm], [w.lam], otr, w.logits, S, B, k, w.beta, w.blank, 1, [[w.V] * H], [0] * H, sc0,
+                       forced_tokens=out["tokens"].cpu().numpy(), forced_parents=out["parents"].cpu().numpy(),
+                       tol=TIE_TOL, threads=threads(), recombine=True)
+    bad = np.nonzero(r["mismatch_at"] >= 0)[0]
+    assert bad.size == 0, f"streams {bad[:5]} diverge at frames {r['mismatch_at'][bad[:5]]}"
+    assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
+    assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
+    fin = np.isfinite(r["hyp_score"])
+    assert np.abs(sc.cpu().numpy()[fin] - r["hyp_score"][fin]).max() <= T * SCORE_TOL

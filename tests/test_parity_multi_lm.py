@@ -237,3 +237,68 @@ def test_end_scores_flag_invalid_states():
     t = term.cpu().numpy()
     assert t[1] == 0.0 and t[2] == 0.0 and t[0] < 0 and t[3] < 0
     assert F.fusion_device_status() == 0  # cleared by the read
+
+
+def test_recombining_beam_exhaustive():
+    """V = 3, T = 3, B = 27, k = 3 with recombination: every distinct history
+    survives (15), and the GPU's merged scores equal the oracle's (the
+    log-sum over each history's alignments)."""
+    V, T, B, k = 3, 3, 27, 3
+    rng = np.random.default_rng(14)
+    lms = [tiny_random_lm(rng, V, 3, n_sent=30), tiny_random_lm(rng, V, 2, n_sent=30)]
+    ph = tiny_random_phrases(rng, V, n=2, max_len=3, alphabet=2)
+    xs = (rng.standard_normal((T, 1, V)) * 2).astype(np.float32)
+    x = np.repeat(xs, B, axis=1)
+    for n in (1, 2):
+        glms = [F.ngram_load_arrays(m) for m in lms[:n]]
+        ls = torch.full((n, B), V, dtype=torch.int32, device=dev())
+        bs = torch.zeros((B,), dtype=torch.int32, device=dev())
+        sc = torch.from_numpy(np.array([0.0] + [-np.inf] * (B - 1))).to(dev())
+        F.run_lms(glms, [0.5, 0.25][:n], F.boost_build_phrases(V, 0, ph), torch.from_numpy(x).to(dev()), 1, B, k,
+                  0.5, 0, F.FUSION_BLANK_COMPETE, ls, bs, sc, recombine=True)
+        torch.cuda.synchronize()
+        assert F.fusion_device_status() == 0
+        r = oracle.run_lms([oracle.OracleLM(m) for m in lms[:n]], [0.5, 0.25][:n], oracle.OracleTrie(V, 0, ph),
+                           x, 1, B, k, 0.5, 0, 1, [[V] * B] * n, [0] * B, recombine=True)
+        got = sc.cpu().numpy()
+        assert np.isfinite(got).sum() == 15
+        assert np.abs(np.sort(got[np.isfinite(got)]) - np.sort(r["hyp_score"][np.isfinite(r["hyp_score"])])).max() \
+            <= T * SCORE_TOL
+
+
+@pytest.mark.parametrize("n_lm", [1, 2])
+def test_recombining_beam_teacher_forced(n_lm):
+    """Beam 4, top-4, 40 frames with recombination: every decision (merged
+    candidates included) is replayed by the oracle, which compares full
+    histories; final states and scores match."""
+    rng = np.random.default_rng(90 + n_lm)
+    V, S, B, k, T = 300, 24, 4, 4, 40
+    lms = [tiny_random_lm(rng, V, 4, n_sent=3000), tiny_random_lm(rng, V, 3, n_sent=2000)][:n_lm]
+    ph = tiny_random_phrases(rng, V, n=40, max_len=4, alphabet=30, with_completion=True)
+    glms = [F.ngram_load_arrays(m) for m in lms]
+    gtr = F.boost_build_phrases(V, 0, ph)
+    H = S * B
+    x = (rng.standard_normal((T, H, V)) * 2).astype(np.float32)
+    x[:, :, 0] += 3
+    alphas = [0.5, 0.25][:n_lm]
+    ls = torch.full((n_lm, H), V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev())
+    sc0 = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)
+    sc = torch.from_numpy(sc0.copy()).to(dev())
+    out = F.run_lms(glms, alphas, gtr, torch.from_numpy(x).to(dev()), S, B, k, 0.5, 0, F.FUSION_BLANK_COMPETE,
+                    ls, bs, sc, recombine=True)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.run_lms([oracle.OracleLM(m) for m in lms], alphas, oracle.OracleTrie(V, 0, ph), x, S, B, k, 0.5,
+                       0, 1, [[V] * H] * n_lm, [0] * H, sc0, forced_tokens=out["tokens"].cpu().numpy(),
+                       forced_parents=out["parents"].cpu().numpy(), tol=TIE_TOL, threads=8, recombine=True)
+    assert (r["mismatch_at"] < 0).all(), f"diverge at {r['mismatch_at'][r['mismatch_at'] >= 0][:5]}"
+    assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
+    assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
+    fin = np.isfinite(r["hyp_score"])
+    assert np.array_equal(np.isfinite(sc.cpu().numpy()), fin)
+    assert np.abs(sc.cpu().numpy()[fin] - r["hyp_score"][fin]).max() <= T * SCORE_TOL
+    # recombination changed the search: the same run without it differs
+    r0 = oracle.run_lms([oracle.OracleLM(m) for m in lms], alphas, oracle.OracleTrie(V, 0, ph), x, S, B, k, 0.5,
+                        0, 1, [[V] * H] * n_lm, [0] * H, sc0, threads=8)
+    assert not np.array_equal(r0["hyp_score"], r["hyp_score"])
