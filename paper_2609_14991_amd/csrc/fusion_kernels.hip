@@ -226,7 +226,8 @@ struct HypState {
 __device__ __forceinline__ constexpr int rec_lane0(int i) { return i == 0 ? 0 : kLM1Lane; }
 
 // MODE: what a launch computes (the code of the other modes is compiled out)
-constexpr int kModeStep = 0, kModeGreedy = 1, kModeBeam = 2;
+// (kModeBeamRC: beam with recombination of equal histories)
+constexpr int kModeStep = 0, kModeGreedy = 1, kModeBeam = 2, kModeBeamRC = 3;
 
 template <int W, int NC, int KM, bool AL, int MODE, int NL>
 __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
@@ -258,8 +259,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   __shared__ int2 s_xb[NL > 1 ? FUSION_MAX_BEAM * FUSION_MAX_K : 1];
   __shared__ int s_xf[FUSION_MAX_BEAM * FUSION_MAX_K];
   __shared__ double s_tot[FUSION_MAX_BEAM * FUSION_MAX_K];
-  __shared__ unsigned long long s_hh[FUSION_MAX_BEAM * FUSION_MAX_K];  // history hash after each candidate
-  __shared__ double s_mt[FUSION_MAX_BEAM * FUSION_MAX_K];              // merged totals (recombination)
+  // recombination: history hash after each candidate, merged totals
+  __shared__ unsigned long long s_hh[MODE == kModeBeamRC ? FUSION_MAX_BEAM * FUSION_MAX_K : 1];
+  __shared__ double s_mt[MODE == kModeBeamRC ? FUSION_MAX_BEAM * FUSION_MAX_K : 1];
   __shared__ long long s_sbase[NL][kMaxLevels];  // state id of arc index i of level L < N-1: s_sbase[L] + i
   __shared__ int s_lbeg[NL][kMaxLevels];  // first arc of each level of the current state
   __shared__ int s_cfg[2];  // V, blank: re-read each frame so per-token masks stay inside the loop
@@ -283,7 +285,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   };
   const int wave = g >> 6;
   const int lane = g & 63;
-  const int B = MODE == kModeBeam ? p.B : 1, K = p.k;
+  constexpr bool BEAM = MODE == kModeBeam || MODE == kModeBeamRC;
+  constexpr bool RC = MODE == kModeBeamRC;
+  const int B = BEAM ? p.B : 1, K = p.k;
   int Nl[NL], RSl[NL];  // order and record stride of each LM
 #pragma unroll
   for (int i = 0; i < NL; ++i) {
@@ -321,7 +325,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     s_steps = 0;
     const int V = p.V, blank = p.blank;
     const int q = p.has_trie ? p.boost_state[h] : 0;
-    const double sc = MODE == kModeBeam ? p.hyp_score[h] : 0.0;
+    const double sc = BEAM ? p.hyp_score[h] : 0.0;
     bool ok_lm = true;
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
@@ -334,17 +338,19 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       hs.cur_lm[i] = sig;
     }
     const bool ok_q = !p.has_trie || (q >= 0 && q < tr.n_nodes);
-    const bool alive = MODE != kModeBeam || sc > -INFINITY;
+    const bool alive = !BEAM || sc > -INFINITY;
     hs.qsrc = q;
     hs.y = -1;
     hs.fl = (alive ? 1 : 0) | ((ok_lm && ok_q) ? 0 : 2);
     hs.cur_q = q;
     hs.S = sc;
-    // the history starts at the slot's initial states
-    unsigned long long hh = mix64(0x243F6A8885A308D3ull ^ (unsigned long long)(unsigned)q);
+    if constexpr (RC) {
+      // the history starts at the slot's initial states
+      unsigned long long hh = mix64(0x243F6A8885A308D3ull ^ (unsigned long long)(unsigned)q);
 #pragma unroll
-    for (int i = 0; i < NL; ++i) hh = mix64(hh ^ ((unsigned long long)(unsigned)hs.lmsrc[i] << (8 * i + 1)));
-    hs.hist = hh & ((1ull << 48) - 1);
+      for (int i = 0; i < NL; ++i) hh = mix64(hh ^ ((unsigned long long)(unsigned)hs.lmsrc[i] << (8 * i + 1)));
+      hs.hist = hh & ((1ull << 48) - 1);
+    }
     if (alive && !(ok_lm && ok_q))
       atomicOr(&g_status, (ok_lm ? 0 : FUSION_STATUS_BAD_LM_STATE) | (ok_q ? 0 : FUSION_STATUS_BAD_BOOST_STATE));
   }
@@ -852,7 +858,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         }
         if (p.has_trie) by += 16ull + 16ull * (unsigned long long)dcnt;
       }
-      by += MODE == kModeBeam ? 8ull : 4ull;
+      by += BEAM ? 8ull : 4ull;
       if (p.fused) by += 4ull * V;
       s_bytes += by;
       s_steps += 1ull;
@@ -987,8 +993,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         // fence).  Frames alternate between two buffers; a writer can be at most
         // one frame ahead of any reader of its stream, so it never overwrites a
         // buffer that is still being read.
-        constexpr int XW = 4 + NL;
-        const int nw = p.recombine ? XW : XW - 1;  // words written and polled
+        constexpr int XW = 3 + NL + (RC ? 1 : 0);
         unsigned long long *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * XW;
         const unsigned long long tag = (unsigned long long)((t + 1) & 0xFFFF) << 48;
         constexpr unsigned long long kPay = (1ull << 48) - 1;
@@ -1003,14 +1008,16 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           w[3] = (unsigned long long)((hs.c1[0] + 1) & 0xFFFF) | ((unsigned long long)(hs.fl & 0xFF) << 16) | tag;
           if constexpr (NL > 1)
             w[4] = (unsigned long long)(unsigned)cl[1] | ((unsigned long long)((hs.c1[1] + 1) & 0xFFFF) << 32) | tag;
-          // the history after the candidate: blank emits nothing
-          const unsigned long long hist = hs.hist;
-          w[XW - 1] = ((!has || cy == blank) ? hist
-                                              : (mix64(hist ^ (0x632BE59BD9B4E019ull * (unsigned long long)(cy + 1))) & kPay)) |
-                      tag;
+          if constexpr (RC) {
+            // the history after the candidate: blank emits nothing
+            const unsigned long long hist = hs.hist;
+            w[XW - 1] = ((!has || cy == blank) ? hist
+                                                : (mix64(hist ^ (0x632BE59BD9B4E019ull * (unsigned long long)(cy + 1))) & kPay)) |
+                        tag;
+          }
 #pragma unroll
           for (int q = 0; q < XW; ++q)
-            if (q < nw) __hip_atomic_store(xs + (b * K + lane) * XW + q, w[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(xs + (b * K + lane) * XW + q, w[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         // every workgroup of the stream ranks the same B*k candidates by (total
         // desc, parent asc, rank asc), i.e. candidate order breaks ties; slot b
@@ -1026,8 +1033,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           for (int spins = 0;; ++spins) {
             if (i < nc) {
 #pragma unroll
-              for (int q = 0; q < XW; ++q)
-                w[q] = q < nw ? __hip_atomic_load(xs + i * XW + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : tag;
+              for (int q = 0; q < XW; ++q) w[q] = __hip_atomic_load(xs + i * XW + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
               cur = true;
 #pragma unroll
               for (int q = 0; q < XW; ++q) cur = cur && (w[q] & ~kPay) == tag;
@@ -1048,7 +1054,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             s_xf[i] = (int)((w[3] >> 16) & 0xFF);
             if constexpr (NL > 1)
               s_xb[i] = make_int2((int)(unsigned)(w[4] & 0xFFFFFFFFull), (int)((w[4] >> 32) & 0xFFFF) - 1);
-            s_hh[i] = w[XW - 1] & kPay;
+            if constexpr (RC) s_hh[i] = w[XW - 1] & kPay;
             s_tot[i] = valid ? __longlong_as_double((long long)((w[0] & kPay) | ((w[1] & 0xFFFF) << 48)))
                              : __longlong_as_double(0x7FF8000000000000ll);
           }
@@ -1056,7 +1062,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-        if (p.recombine) {
+        if constexpr (RC) {
           // recombination: candidates that reach the same history (equal hash)
           // merge into the first of them in candidate order, with the log-sum
           // of their totals folded in that order; the others leave the ranking
@@ -1128,7 +1134,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           hs.qsrc = a.z;
           hs.y = y;
           hs.fl = 1 | (s_xf[wi] & 2);
-          hs.hist = s_hh[wi];
+          if constexpr (RC) hs.hist = s_hh[wi];
           hs.S = s_tot[wi];
           p.tokens[o] = y;
           p.parents[o] = wi / K;
@@ -1167,7 +1173,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     }
     if (moved && nq < 0) nq = tr.root_node[y].w;
     if (p.has_trie) p.boost_state[h] = nq;
-    if (MODE == kModeBeam) p.hyp_score[h] = hs.S;
+    if (BEAM) p.hyp_score[h] = hs.S;
   }
   if (p.traffic && g == 0) {
     const unsigned long long extra = (h == 0 && p.has_trie) ? 4ull * p.V * (unsigned long long)p.T : 0ull;
@@ -1190,6 +1196,7 @@ KernelFn pick_mode(int mode) {
   if constexpr (KM == 1) {
     if (mode == kModeGreedy) return fusion_kernel<W, NC, KM, AL, kModeGreedy, NL>;
   }
+  if (mode == kModeBeamRC) return fusion_kernel<W, NC, KM, AL, kModeBeamRC, NL>;
   return mode == kModeStep ? fusion_kernel<W, NC, KM, AL, kModeStep, NL> : fusion_kernel<W, NC, KM, AL, kModeBeam, NL>;
 }
 template <int W, int NC, int KM, int NL>
@@ -1260,7 +1267,7 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   const Shape sh = shape_for(p.V);
   const int km = p.k <= 1 ? 1 : p.k <= 4 ? 4 : 8;
   const bool al = (p.V % 4 == 0) && ((uintptr_t)p.logits % 16 == 0) && (!p.fused || (uintptr_t)p.fused % 16 == 0);
-  const int mode = p.step_mode ? kModeStep : p.B == 1 ? kModeGreedy : kModeBeam;
+  const int mode = p.step_mode ? kModeStep : p.B == 1 ? kModeGreedy : p.recombine ? kModeBeamRC : kModeBeam;
   KernelFn fn = pick(sh, km, al, mode, p.n_lm);
   if (!fn) return set_error(FUSION_E_UNSUPPORTED, "two LMs need V <= 4096");
   const DeviceInfo di = device_info();
@@ -1289,8 +1296,8 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   int s_batch = (int)std::min<long>(p.S, resident / p.B);
   if (s_batch >= 8) s_batch -= s_batch % 8;
   if (s_batch < 1) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device at once");
-  // exchange records: 2 buffers x B x k candidates x (4 + n_lm) words per stream
-  const size_t xwords = (size_t)s_batch * 2 * p.B * p.k * (4 + p.n_lm);
+  // exchange records: 2 buffers x B x k candidates x (3 + n_lm (+1 recombining)) words per stream
+  const size_t xwords = (size_t)s_batch * 2 * p.B * p.k * (3 + p.n_lm + (p.recombine ? 1 : 0));
   void *scratch = nullptr;
   e = hipMallocAsync(&scratch, xwords * sizeof(unsigned long long), stream);
   if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
