@@ -86,6 +86,7 @@ def main():
     ap.add_argument("--fused", action="store_true", help="also write the full fused score rows")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-projection", action="store_true", help="skip the joint-projection measurement")
+    ap.add_argument("--no-recombine", action="store_true", help="skip the recombining-beam measurement")
     ap.add_argument("--no-second-lm", action="store_true",
                     help="skip the two-LM measurement (C5 with a second, keyword 4-gram LM)")
     ap.add_argument("--cpu-frames", type=int, default=300)
@@ -309,6 +310,50 @@ def main():
             else "no PMC record for these kernel sources")
         log(f"two LMs: {k2:.3f} ms kernel, {alg2 / max(steps2, 1):.0f} B/hyp-step, {ach2:.1f} GB/s")
         del lm2
+
+    # the same decode with beam recombination (candidates that reach the same
+    # history merge, log-summed): the kernel's recombining beam variant
+    if not args.no_recombine and B > 1:
+        ls1 = ls0.view(1, H)
+        lsr = ls1.clone()
+
+        def run_rc(traffic=None):
+            lsr.copy_(ls1)
+            bs.copy_(bs0)
+            sc.copy_(sc0)
+            F.fusion_run_lms([lm], [w.lam], trie, x, T, S, B, V, k, w.beta, w.blank, mode, lsr, bs, sc, tokens,
+                             parents, None, traffic, flags=F.FUSION_RUN_RECOMBINE, stream=stream.cuda_stream)
+
+        traffic3 = torch.zeros(2, dtype=torch.int64, device=dev)
+        run_rc(traffic3)
+        torch.cuda.synchronize()
+        assert F.fusion_device_status() == 0
+        alg3, steps3 = (int(v) for v in traffic3.cpu())
+        for _ in range(2):
+            run_rc()
+        n3 = max(3, args.steps // 4)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n3)]
+        torch.cuda.synchronize()
+        for a, b in ev:
+            lsr.copy_(ls1)
+            bs.copy_(bs0)
+            sc.copy_(sc0)
+            a.record(stream)
+            F.fusion_run_lms([lm], [w.lam], trie, x, T, S, B, V, k, w.beta, w.blank, mode, lsr, bs, sc, tokens,
+                             parents, None, None, flags=F.FUSION_RUN_RECOMBINE, stream=stream.cuda_stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        k3 = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+        ach3 = alg3 / (k3 / 1e3) / 1e9
+        out["recombining_beam"] = {
+            "kernel": "fusion_kernel (beam with recombination)", "launches": n3, "kernel_ms_per_launch": k3,
+            "value": float(T) * H * V / (k3 / 1e3), "unit": "hyp×vocab scores/s",
+            "decode_steps_per_s": T / (k3 / 1e3),
+            "roofline": {"bound": "hbm", "achieved": ach3, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": ach3 / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg3,
+                         "bytes_per_hyp_step": alg3 / max(steps3, 1), "traffic": None},
+        }
+        log(f"recombining beam: {k3:.3f} ms kernel, {alg3 / max(steps3, 1):.0f} B/hyp-step, {ach3:.1f} GB/s")
 
     rec = recorded_traffic(w.name)
     digest = kernel_sources_digest()
