@@ -41,6 +41,7 @@ KERNEL_SOURCES = ("paper_2609_14991_amd/csrc/fusion_kernels.hip", "paper_2609_14
                   "paper_2609_14991_amd/csrc/ngram_tables.cpp", "paper_2609_14991_amd/csrc/boost_trie.cpp")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fusion_kernel_c5_hbm_traffic.md")
 TRAFFIC_FILE_TWO_LMS = os.path.join(ROOT, "profiles", "fusion_kernel_c5_two_lms_hbm_traffic.md")
+TRAFFIC_FILE_RC = os.path.join(ROOT, "profiles", "fusion_kernel_c5_recombining_hbm_traffic.md")
 
 
 def kernel_sources_digest():
@@ -351,8 +352,14 @@ def main():
             "decode_steps_per_s": T / (k3 / 1e3),
             "roofline": {"bound": "hbm", "achieved": ach3, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": ach3 / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg3,
-                         "bytes_per_hyp_step": alg3 / max(steps3, 1), "traffic": None},
+                         "bytes_per_hyp_step": alg3 / max(steps3, 1)},
         }
+        rec3 = recorded_traffic(w.name + "+recombine", TRAFFIC_FILE_RC)
+        ok3 = rec3 is not None and rec3[1] == kernel_sources_digest()
+        out["recombining_beam"]["roofline"]["traffic"] = rec3[0] if ok3 else None
+        out["recombining_beam"]["roofline"]["traffic_note"] = (
+            "HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)" if ok3
+            else "no PMC record for these kernel sources")
         log(f"recombining beam: {k3:.3f} ms kernel, {alg3 / max(steps3, 1):.0f} B/hyp-step, {ach3:.1f} GB/s")
 
     rec = recorded_traffic(w.name)
