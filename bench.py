@@ -9,6 +9,9 @@ Prints one JSON line: hyp x vocab scores/s (value), decode steps/s, the
 roofline of the fusion kernel (algorithmic bytes per launch / mean launch
 time from HIP events) and the CPU oracle timed on a bounded sample of the
 same workload, whose decisions are also checked against the GPU trajectory.
+Beside the main step it times the joint output projection, the decode with a
+second LM, the recombining beam and the keyword workload (the steering
+conditions of Table II on synthetic terms and logits), each in its own object.
 """
 
 from __future__ import annotations
@@ -78,6 +81,75 @@ def copy_probe(nbytes):
     log(f"copied {n * 4} bytes 3 times")
 
 
+def keyword_leg(F, torch, dev, stream, n_launch):
+    """The keyword workload: 285 test streams decoded greedily under each
+    steering condition of Table II (keyword recall and token error rate from
+    the GPU's tokens), then the deployed set-up (keyword-synth 4-gram and
+    phrase boost together) timed with HIP events."""
+    from workloads import CONDITIONS, hypotheses, keyword_recall, make_keyword_workload, token_error_rate
+
+    t0 = time.time()
+    kw = make_keyword_workload()
+    glms = {k: F.ngram_load_arrays(kw.lm(k)) for k in ("general", "keyword", "refs")}
+    gtr = F.boost_build_phrases(kw.V, kw.blank, kw.phrases)
+    log(f"keyword workload {kw.name}: {kw.S} streams x {kw.T} frames, built in {time.time() - t0:.1f}s")
+    x = torch.from_numpy(kw.logits).to(dev)
+    S, T, V = kw.S, kw.T, kw.V
+    ls = torch.empty((S,), dtype=torch.int32, device=dev)
+    bs = torch.empty((S,), dtype=torch.int32, device=dev)
+    tokens = torch.empty((T, S), dtype=torch.int32, device=dev)
+
+    def decode(lm, alpha, beta, traffic=None):
+        ls.fill_(F.ngram_bos_state(lm))
+        bs.zero_()
+        F.fusion_run(lm, gtr, x, T, S, 1, V, 1, alpha, beta, kw.blank, F.FUSION_BLANK_AM, ls, bs, None, tokens,
+                     None, None, traffic, stream.cuda_stream)
+
+    conds = list(CONDITIONS) + [("ngram_keyword_synth+phrase_boost", "keyword", kw.lam, kw.beta)]
+    table = {}
+    for name, which, alpha, beta in conds:
+        decode(glms[which or "general"], alpha, beta)
+        torch.cuda.synchronize()
+        assert F.fusion_device_status() == 0
+        hy = hypotheses(tokens.cpu().numpy(), kw.blank)
+        r, hit, tot = keyword_recall(hy, kw.ref_terms, kw.terms)
+        table[name] = {"alpha": alpha, "beta": beta, "recall": r, "terms_found": hit, "terms": tot,
+                       "token_error_rate": token_error_rate(hy, kw.refs)}
+    lm = glms["keyword"]
+    traffic = torch.zeros(2, dtype=torch.int64, device=dev)
+    decode(lm, kw.lam, kw.beta, traffic)
+    torch.cuda.synchronize()
+    alg, steps = (int(v) for v in traffic.cpu())
+    for _ in range(2):
+        decode(lm, kw.lam, kw.beta)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_launch)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        ls.fill_(F.ngram_bos_state(lm))
+        bs.zero_()
+        a.record(stream)
+        F.fusion_run(lm, gtr, x, T, S, 1, V, 1, kw.lam, kw.beta, kw.blank, F.FUSION_BLANK_AM, ls, bs, None, tokens,
+                     None, None, None, stream.cuda_stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    kms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    ach = alg / (kms / 1e3) / 1e9
+    log(f"keyword workload: {kms:.3f} ms kernel, {alg / max(steps, 1):.0f} B/hyp-step, {ach:.1f} GB/s; recall " +
+        ", ".join(f"{n} {v['recall']:.3f}" for n, v in table.items()))
+    return {
+        "workload": kw.name, "streams": S, "frames": T, "V": V, "lm_order": kw.N,
+        "ngrams": {k: int(sum(kw.lm(k).counts)) for k in ("general", "keyword", "refs")},
+        "terms": len(kw.terms), "data": "synthetic (terms, templates, transcripts and logits drawn from seeds)",
+        "conditions": table,
+        "timed": "ngram_keyword_synth+phrase_boost", "launches": n_launch, "kernel_ms_per_launch": kms,
+        "value": float(T) * S * V / (kms / 1e3), "unit": "hyp×vocab scores/s",
+        "decode_steps_per_s": T / (kms / 1e3),
+        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": ach / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg,
+                     "bytes_per_hyp_step": alg / max(steps, 1), "traffic": None},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -90,6 +162,8 @@ def main():
     ap.add_argument("--no-recombine", action="store_true", help="skip the recombining-beam measurement")
     ap.add_argument("--no-second-lm", action="store_true",
                     help="skip the two-LM measurement (C5 with a second, keyword 4-gram LM)")
+    ap.add_argument("--no-keyword", action="store_true",
+                    help="skip the keyword workload (steering conditions of Table II, synthetic)")
     ap.add_argument("--cpu-frames", type=int, default=300)
     ap.add_argument("--cpu-streams", type=int, default=64)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -361,6 +435,9 @@ def main():
             "HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)" if ok3
             else "no PMC record for these kernel sources")
         log(f"recombining beam: {k3:.3f} ms kernel, {alg3 / max(steps3, 1):.0f} B/hyp-step, {ach3:.1f} GB/s")
+
+    if not args.no_keyword:
+        out["keyword_workload"] = keyword_leg(F, torch, dev, stream, max(3, args.steps // 4))
 
     rec = recorded_traffic(w.name)
     digest = kernel_sources_digest()

@@ -23,3 +23,14 @@ from .gen import (  # noqa: F401
     tiny_random_lm,
     tiny_random_phrases,
 )
+from .keyword import (  # noqa: F401,E402
+    KEYWORD,
+    CONDITIONS,
+    KeywordWorkload,
+    make_keyword_workload,
+    hypotheses,
+    keyword_recall,
+    token_error_rate,
+    edit_distance,
+    count_occurrences,
+)
