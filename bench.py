@@ -45,6 +45,7 @@ KERNEL_SOURCES = ("paper_2609_14991_amd/csrc/fusion_kernels.hip", "paper_2609_14
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fusion_kernel_c5_hbm_traffic.md")
 TRAFFIC_FILE_TWO_LMS = os.path.join(ROOT, "profiles", "fusion_kernel_c5_two_lms_hbm_traffic.md")
 TRAFFIC_FILE_RC = os.path.join(ROOT, "profiles", "fusion_kernel_c5_recombining_hbm_traffic.md")
+TRAFFIC_FILE_KW = os.path.join(ROOT, "profiles", "fusion_kernel_keyword_hbm_traffic.md")
 
 
 def kernel_sources_digest():
@@ -136,6 +137,8 @@ def keyword_leg(F, torch, dev, stream, n_launch):
     ach = alg / (kms / 1e3) / 1e9
     log(f"keyword workload: {kms:.3f} ms kernel, {alg / max(steps, 1):.0f} B/hyp-step, {ach:.1f} GB/s; recall " +
         ", ".join(f"{n} {v['recall']:.3f}" for n, v in table.items()))
+    rec = recorded_traffic(kw.name, TRAFFIC_FILE_KW)
+    ok = rec is not None and rec[1] == kernel_sources_digest()
     return {
         "workload": kw.name, "streams": S, "frames": T, "V": V, "lm_order": kw.N,
         "ngrams": {k: int(sum(kw.lm(k).counts)) for k in ("general", "keyword", "refs")},
@@ -146,7 +149,9 @@ def keyword_leg(F, torch, dev, stream, n_launch):
         "decode_steps_per_s": T / (kms / 1e3),
         "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": ach / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg,
-                     "bytes_per_hyp_step": alg / max(steps, 1), "traffic": None},
+                     "bytes_per_hyp_step": alg / max(steps, 1), "traffic": rec[0] if ok else None,
+                     "traffic_note": ("HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)"
+                                      if ok else "no PMC record for these kernel sources")},
     }
 
 
