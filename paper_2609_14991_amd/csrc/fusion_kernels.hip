@@ -173,6 +173,13 @@ template <int CTRL, int ROWS>
 __device__ __forceinline__ int dpp_i(int v) {
   return __builtin_amdgcn_update_dpp(INT_MIN, v, CTRL, ROWS, 0xF, false);
 }
+// maximum of an int over each 16-lane row, in every lane of the row
+__device__ __forceinline__ int row_max_i(int v) {
+  v = max(v, dpp_i<0xB1, 0xF>(v));
+  v = max(v, dpp_i<0x4E, 0xF>(v));
+  v = max(v, dpp_i<0x141, 0xF>(v));
+  return max(v, dpp_i<0x140, 0xF>(v));
+}
 __device__ __forceinline__ int wave_max_i(int v) {
   v = max(v, dpp_i<0xB1, 0xF>(v));
   v = max(v, dpp_i<0x4E, 0xF>(v));
@@ -252,6 +259,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   __shared__ int s_paid[kMaxWaves];
   __shared__ int w_key[kMaxWaves][KM];  // order-preserving images of the keys (ord_key)
   __shared__ int w_y[kMaxWaves][KM];
+  __shared__ int s_wmax[kMaxWaves];  // each wave's best key (KM > 1)
   __shared__ HypState<NL> hs;
   // beam rendezvous staging (wave 0): candidate records (the second LM's source
   // and c_1 in s_xb), parent flags, totals
@@ -693,18 +701,20 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const bool write_fused = p.fused != nullptr && ok;
     const rsrc_t fr = row_rsrc(write_fused ? p.fused + rowoff : p.logits, write_fused ? V : 0);
     float kk[NC][4];
-    uint32_t vm = 0u;  // bit c*4+j: token (c, j) of this lane is still a candidate
+    bool cd[NC][4];  // token (c, j) of this lane is a candidate
+    // which tokens compete this frame (uniform): blank in blank-only frames or
+    // when it competes, the others unless the frame is blank-only
+    const bool take_blank = act & (blank_only | compete);
+    const bool take_other = act & !blank_only;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int y0 = (c * W + g) * 4;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        // candidates: live tokens; blank only in blank-only frames or when it competes
-        // (bitwise logic: no per-token branches)
+        // bitwise logic on lane masks: no per-token branches
         const int y = y0 + j;
         const bool is_blank = y == blank;
-        const bool cand = act & (y < V) & (blank_only ? is_blank : (compete | !is_blank));
-        vm |= (uint32_t)cand << (c * 4 + j);
+        cd[c][j] = (y < V) & ((is_blank & take_blank) | (!is_blank & take_other));
         kk[c][j] = xv[c][j];
       }
       if (want_keys) {
@@ -801,9 +811,76 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 #pragma unroll
       for (int c = 0; c < NC; ++c)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) sk[c][j] = ((vm >> (c * 4 + j)) & 1u) ? ord_key(kk[c][j]) : INT_MIN;
+        for (int j = 0; j < 4; ++j) {
+          const int o = ord_key(kk[c][j]);
+          sk[c][j] = cd[c][j] ? o : INT_MIN;
+        }
+      // With K > 1 the rounds below run only in a wave that holds more than K
+      // keys at or above tau, the K-th largest of the NW wave maxima: those
+      // maxima are K distinct tokens with keys >= tau, so no key below tau is
+      // among the hypothesis' top K.  A wave with at most K such keys writes
+      // them straight into its list (any order: the hypothesis' top-k ranks
+      // by key, then id).
+      bool listed = false;
+      if constexpr (KM > 1) {
+        int lb = INT_MIN;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) lb = max(lb, max(max(sk[c][0], sk[c][1]), max(sk[c][2], sk[c][3])));
+        const int mw = wave_max_i(lb);
+        if (lane == 0) s_wmax[wave] = mw;
+        lds_barrier();
+        int tau = INT_MIN;
+        if (NW >= K) {
+          // lanes 0..NW-1 (one row) hold the maxima; K-1 rounds each drop one
+          // instance of the row maximum, then the maximum left is the K-th largest
+          int v = lane < NW ? s_wmax[lane] : INT_MIN;
+          for (int r = 0; r + 1 < K; ++r) {
+            const int m = row_max_i(v);
+            const unsigned long long own = __ballot(v == m) & 0xFFFFull;
+            v = lane == __ffsll((long long)own) - 1 ? INT_MIN : v;
+          }
+          tau = __builtin_amdgcn_readlane(row_max_i(v), 0);
+        }
+        // survivors: keys >= tau, never a non-candidate (INT_MIN; every real key,
+        // -inf included, maps above it)
+        const int thr = max(tau, INT_MIN + 1);
+        unsigned long long sb[NC][4];
+        int n = 0;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            sb[c][j] = __ballot(sk[c][j] >= thr);
+            n += __popcll(sb[c][j]);
+          }
+        if (n <= K) {
+          int base = 0;
+#pragma unroll
+          for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              if (sk[c][j] >= thr) {
+                const int slot = base + __builtin_amdgcn_mbcnt_hi((uint32_t)(sb[c][j] >> 32),
+                                                                  __builtin_amdgcn_mbcnt_lo((uint32_t)sb[c][j], 0u));
+                w_key[wave][slot] = sk[c][j];
+                w_y[wave][slot] = (c * W + wave * 64 + lane) * 4 + j;
+              }
+              base += __popcll(sb[c][j]);
+            }
+          if (lane >= n && lane < K) {
+            w_key[wave][lane] = INT_MIN;
+            w_y[wave][lane] = INT_MAX;
+          }
+          listed = true;
+        } else {
+#pragma unroll
+          for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) sk[c][j] = sk[c][j] >= thr ? sk[c][j] : INT_MIN;
+        }
+      }
       int rk = INT_MIN, ry = INT_MAX;  // lane r: entry r of the wave's list
-      for (int r = 0; r < K; ++r) {
+      for (int r = 0; r < (listed ? 0 : K); ++r) {
         int lbc[NC];
         int lb = INT_MIN;
 #pragma unroll
@@ -840,7 +917,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         rk = lane == r ? M : rk;
         ry = lane == r ? wy : ry;
       }
-      if (lane < K) {
+      if (!listed && lane < K) {
         w_key[wave][lane] = rk;
         w_y[wave][lane] = ry;
       }
