@@ -141,7 +141,9 @@ void boost_free(BoostTrie *t);
  *   lm, trie     handles (trie NULL: the beta term is 0)
  *   logits       device [H, V] fp32, row-major (joint output of this frame)
  *   lm_state     device [H] LM state ids;  boost_state device [H] phrase state ids
- *   H            1..2^24;  V must equal the handles' vocab
+ *   H            0..2^24;  V must equal the handles' vocab.  H == 0 checks
+ *                the scalar arguments and handles and returns FUSION_OK
+ *                without reading or writing any buffer
  *   lambda, beta fusion weights of Eq. (1)
  *   k            1..FUSION_MAX_K candidates per hypothesis (k <= V)
  *   blank_mode   FUSION_BLANK_AM (requires k == 1) or FUSION_BLANK_COMPETE
@@ -183,9 +185,9 @@ int fusion_step(const NgramTables *lm, const BoostTrie *trie, const float *logit
  *                and a dense row, phrase rows, outputs) and the number of
  *                hypothesis-steps processed
  * States carry across calls, so a stream can be decoded chunk by chunk with
- * the same result as one call over all frames.  T == 0 checks the scalar
- * arguments and handles and returns FUSION_OK without reading or writing any
- * buffer (logits and outputs may then be NULL).
+ * the same result as one call over all frames.  T == 0 or S == 0 checks the
+ * scalar arguments and handles and returns FUSION_OK without reading or
+ * writing any buffer (logits and outputs may then be NULL).
  */
 int fusion_run(const NgramTables *lm, const BoostTrie *trie, const float *logits, int32_t T,
                int32_t S, int32_t B, int32_t V, int32_t k, float lambda, float beta,

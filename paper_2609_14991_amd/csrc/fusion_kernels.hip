@@ -260,13 +260,15 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   __shared__ int w_key[kMaxWaves][KM];  // order-preserving images of the keys (ord_key)
   __shared__ int w_y[kMaxWaves][KM];
   __shared__ int s_wmax[kMaxWaves];  // each wave's best key (KM > 1)
+  __shared__ __align__(16) int2 s_sel[16];  // the hypothesis' listed entries (key, id), compacted
+  __shared__ int2 s_win[KM];                // its top K by rank
   __shared__ HypState<NL> hs;
   // beam rendezvous staging (wave 0): candidate records (the second LM's source
   // and c_1 in s_xb), parent flags, totals
   __shared__ int4 s_xa[FUSION_MAX_BEAM * FUSION_MAX_K];
   __shared__ int2 s_xb[NL > 1 ? FUSION_MAX_BEAM * FUSION_MAX_K : 1];
   __shared__ int s_xf[FUSION_MAX_BEAM * FUSION_MAX_K];
-  __shared__ double s_tot[FUSION_MAX_BEAM * FUSION_MAX_K];
+  __shared__ __align__(16) double s_tot[FUSION_MAX_BEAM * FUSION_MAX_K];
   // recombination: history hash after each candidate, merged totals
   __shared__ unsigned long long s_hh[MODE == kModeBeamRC ? FUSION_MAX_BEAM * FUSION_MAX_K : 1];
   __shared__ double s_mt[MODE == kModeBeamRC ? FUSION_MAX_BEAM * FUSION_MAX_K : 1];
@@ -961,7 +963,45 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
       // candidate j ends in lane j
       int ck = INT_MIN, cy = INT_MAX;
-      for (int j = 0; j < K; ++j) {
+      bool picked = false;
+      if constexpr (kSlots == 1 && KM > 1 && !RC) {  // (no registers to spare with recombination)
+        // at most 16 listed entries (the usual case after the wave-level
+        // narrowing): compact them into LDS, let each count the entries ahead
+        // of it (key desc, then id asc) in registers, and place it by that rank
+        const bool valid = ek[0] != INT_MIN;
+        const unsigned long long vb = __ballot(valid);
+        const int n = __popcll(vb);
+        if (n <= 16) {
+          const int pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(vb >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)vb, 0u));
+          if (valid) s_sel[pos] = make_int2(ek[0], ey[0]);
+          if (lane >= n && lane < 16) s_sel[lane] = make_int2(INT_MIN, INT_MAX);
+          // one wave: its LDS operations complete in order
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          int kv[16], yv[16];
+#pragma unroll
+          for (int q = 0; q < 16; q += 2) {
+            const int4 d = *reinterpret_cast<const int4 *>(&s_sel[q]);
+            kv[q] = d.x;
+            yv[q] = d.y;
+            kv[q + 1] = d.z;
+            yv[q + 1] = d.w;
+          }
+          const int2 me = s_sel[lane & 15];
+          int r = 0;
+#pragma unroll
+          for (int q = 0; q < 16; ++q) r += (int)((kv[q] > me.x) | ((kv[q] == me.x) & (yv[q] < me.y)));
+          if (lane < n && r < K) s_win[r] = me;
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          const int nk = min(n, K);
+          const int2 wv = s_win[lane < nk ? lane : 0];
+          if (lane < nk) {
+            ck = wv.x;
+            cy = wv.y;
+          }
+          picked = true;
+        }
+      }
+      for (int j = 0; j < (picked ? 0 : K); ++j) {
         int v = ek[0];
 #pragma unroll
         for (int q = 1; q < kSlots; ++q) v = max(v, ek[q]);
@@ -1134,6 +1174,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             if constexpr (RC) s_hh[i] = w[XW - 1] & kPay;
             s_tot[i] = valid ? __longlong_as_double((long long)((w[0] & kPay) | ((w[1] & 0xFFFF) << 48)))
                              : __longlong_as_double(0x7FF8000000000000ll);
+          } else if (i < 16) {
+            s_tot[i] = __longlong_as_double(0x7FF8000000000000ll);  // unused: never ahead
           }
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -1177,7 +1219,33 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
         }
         int wi = -1;
-        for (int i = lane; i < nc; i += 64) {
+        bool ranked = false;
+        if (!RC && nc <= 16) {  // (the recombining variant has no registers to spare)
+          // up to 16 candidates (B * k <= 16; entries nc..15 hold NaN): every
+          // lane loads all totals at once (eight 16-byte reads) and counts
+          // those ahead of its own in registers; equal totals need the
+          // candidate-order rule and take the general count below
+          double tv[16];
+#pragma unroll
+          for (int q = 0; q < 16; q += 2) {
+            const double2 d = *reinterpret_cast<const double2 *>(&s_tot[q]);
+            tv[q] = d.x;
+            tv[q + 1] = d.y;
+          }
+          const double ti = s_tot[lane & 15];
+          int gt = 0, eq = 0;
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            gt += (int)(tv[q] > ti);
+            eq += (int)(tv[q] == ti);
+          }
+          const bool live = lane < nc && ti == ti;
+          if (__ballot(live && eq > 1) == 0ull) {
+            if (live && gt == b) wi = lane;
+            ranked = true;
+          }
+        }
+        for (int i = (ranked ? 64 : 0) + lane; i < nc; i += 64) {
           const double ti = s_tot[i];
           if (ti == ti) {
             int r = 0;
@@ -1442,9 +1510,10 @@ int step_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, 
               const float *logits, const int32_t *lm_state, const int32_t *boost_state, int32_t H, int32_t V,
               float beta, int32_t blank_id, int32_t k, int32_t blank_mode, float *fused, int32_t *tokens,
               float *scores, int32_t *next_lm, int32_t *next_boost, hipStream_t stream) {
-  int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta);
+  int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta, H != 0);
   if (rc != FUSION_OK) return rc;
-  if (H < 1 || H > (1 << 24)) return set_error(FUSION_E_ARG, "H out of range");
+  if (H < 0 || H > (1 << 24)) return set_error(FUSION_E_ARG, "H out of range");
+  if (H == 0) return FUSION_OK;  // no hypotheses: no buffer is read or written
   if (!lm_state || !tokens || !scores || !next_lm || !next_boost || (trie && !boost_state))
     return set_error(FUSION_E_ARG, "NULL state or output buffer");
   Params p = make_params(lms, alphas, n_lm, trie);
@@ -1472,14 +1541,14 @@ int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, c
              const float *logits, int32_t T, int32_t S, int32_t B, int32_t V, int32_t k, float beta,
              int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state, double *hyp_score,
              int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, int32_t flags, hipStream_t stream) {
-  int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta, T != 0);
+  int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta, T != 0 && S != 0);
   if (rc != FUSION_OK) return rc;
-  if (T < 0 || S < 1 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
+  if (T < 0 || S < 0 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
   if ((int64_t)S * B > (1 << 24)) return set_error(FUSION_E_ARG, "too many hypotheses");
   if (B == 1 && k != 1) return set_error(FUSION_E_ARG, "greedy decoding (B == 1) needs k == 1");
   if (B > 1 && blank_mode != FUSION_BLANK_COMPETE) return set_error(FUSION_E_ARG, "beam decoding needs FUSION_BLANK_COMPETE");
   if (flags & ~FUSION_RUN_RECOMBINE) return set_error(FUSION_E_ARG, "unknown flags");
-  if (T == 0) return FUSION_OK;  // nothing to decode: no buffer is read or written
+  if (T == 0 || S == 0) return FUSION_OK;  // nothing to decode: no buffer is read or written
   if (!lm_state || !tokens || (trie && !boost_state)) return set_error(FUSION_E_ARG, "NULL state or output buffer");
   if (B > 1 && (!hyp_score || !parents)) return set_error(FUSION_E_ARG, "beam decoding needs hyp_score and parents");
   Params p = make_params(lms, alphas, n_lm, trie);

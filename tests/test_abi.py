@@ -117,6 +117,12 @@ def test_fusion_calls_reject_bad_arguments(lib):
                         None, None, None, None)
     assert rc == F.FUSION_E_ARG
     assert "NULL" in F.fusion_last_error()
+    # an empty batch still needs valid handles
+    rc = lib.fusion_step(None, None, None, None, None, 0, 4, 0.5, 0.5, 0, 1, 0, *out, None)
+    assert rc == F.FUSION_E_ARG
+    rc = lib.fusion_run(None, None, None, 1, 0, 1, 4, 1, 0.5, 0.5, 0, 0, None, None, None, None,
+                        None, None, None, None)
+    assert rc == F.FUSION_E_ARG
 
 
 def test_several_lm_calls_reject_bad_arguments(lib):

@@ -132,3 +132,21 @@ def test_zero_frames_change_nothing():
     assert out["tokens"].numel() == 0
     assert (ls.cpu().numpy() == 130).all() and (bs.cpu().numpy() == 0).all()
     assert sc.cpu().numpy()[0] == 0.0 and sc.cpu().numpy()[2] == -1.5
+
+
+def test_empty_batches_touch_nothing():
+    """H == 0 (step) and S == 0 (run) check the handles and scalars, then
+    return without reading or writing a buffer; bad scalars still fail."""
+    rng, lm, ph = models(130, 4)
+    glm, gtr = F.ngram_load_arrays(lm), F.boost_build_phrases(130, 0, ph)
+    e32 = torch.empty((0,), dtype=torch.int32, device=dev())
+    g = F.step(glm, gtr, torch.empty((0, 130), device=dev()), e32, e32, 0.5, 0.5, 0, 4, 1)
+    assert g["tokens"].shape == (0, 4)
+    x = torch.empty((5, 0, 130), device=dev())
+    out = F.run(glm, gtr, x, 0, 4, 4, 0.5, 0.5, 0, F.FUSION_BLANK_COMPETE, e32, e32,
+                torch.empty((0,), dtype=torch.float64, device=dev()))
+    assert out["tokens"].shape == (5, 0)
+    with pytest.raises(F.FusionError):
+        F.step(glm, gtr, torch.empty((0, 130), device=dev()), e32, e32, 0.5, 0.5, 0, 0, 1)  # k = 0
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
