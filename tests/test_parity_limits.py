@@ -150,3 +150,33 @@ def test_empty_batches_touch_nothing():
         F.step(glm, gtr, torch.empty((0, 130), device=dev()), e32, e32, 0.5, 0.5, 0, 0, 1)  # k = 0
     torch.cuda.synchronize()
     assert F.fusion_device_status() == 0
+
+
+@pytest.mark.parametrize("lam_beta", [(0.0, 0.0), (0.5, 0.5)])
+def test_beam_exact_ties(lam_beta):
+    """Integer-valued logits make many fused scores, and so many candidate
+    totals, exactly equal: the beam's ranking must break them by candidate
+    order (parent, then rank) and the top-k by token id, as the oracle does,
+    in free-running decoding (no replay)."""
+    lam, beta = lam_beta
+    V, S, B, k, T = 130, 3, 4, 4, 12
+    rng, lm, ph = models(V, 11)
+    glm, gtr = F.ngram_load_arrays(lm), F.boost_build_phrases(V, 0, ph)
+    x = rng.integers(-2, 3, size=(T, S * B, V)).astype(np.float32)
+    H = S * B
+    ls = torch.full((H,), V, dtype=torch.int32, device=dev())
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev())
+    sc0 = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)
+    sc = torch.from_numpy(sc0.copy()).to(dev())
+    out = F.run(glm, gtr, torch.from_numpy(x).to(dev()), S, B, k, lam, beta, 0, F.FUSION_BLANK_COMPETE, ls, bs, sc)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.run(oracle.OracleLM(lm), oracle.OracleTrie(V, 0, ph), x, S, B, k, lam, beta, 0, 1, [V] * H, [0] * H,
+                   sc0)
+    assert np.array_equal(out["tokens"].cpu().numpy(), r["tokens"])
+    assert np.array_equal(out["parents"].cpu().numpy(), r["parents"])
+    assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
+    assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
+    fin = np.isfinite(r["hyp_score"])
+    assert np.array_equal(np.isfinite(sc.cpu().numpy()), fin)
+    assert np.abs(sc.cpu().numpy()[fin] - r["hyp_score"][fin]).max() <= T * SCORE_TOL
