@@ -82,6 +82,42 @@ def copy_probe(nbytes):
     log(f"copied {n * 4} bytes 3 times")
 
 
+def time_leg(F, torch, dev, stream, reset, launch, n_launch):
+    """One launch with the kernel's byte count on (algorithmic bytes and
+    hypothesis-steps), two warm-up launches, then the mean HIP-event time of
+    n_launch launches on `stream`; `reset()` restores the carried state before
+    each launch, outside the events."""
+    traffic = torch.zeros(2, dtype=torch.int64, device=dev)
+    reset()
+    launch(traffic)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    alg, steps = (int(v) for v in traffic.cpu())
+    for _ in range(2):
+        reset()
+        launch(None)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_launch)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        reset()
+        a.record(stream)
+        launch(None)
+        b.record(stream)
+    torch.cuda.synchronize()
+    return alg, steps, float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+
+def leg_roofline(alg, steps, kms, record):
+    """The roofline object of a leg; `record` is its PMC traffic record or None."""
+    ach = alg / (kms / 1e3) / 1e9
+    ok = record is not None and record[1] == kernel_sources_digest()
+    return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+            "algorithmic_bytes_per_launch": alg, "bytes_per_hyp_step": alg / max(steps, 1),
+            "traffic": record[0] if ok else None,
+            "traffic_note": ("HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)" if ok
+                             else "no PMC record for these kernel sources")}
+
+
 def keyword_leg(F, torch, dev, stream, n_launch):
     """The keyword workload: 285 test streams decoded greedily under each
     steering condition of Table II (keyword recall and token error rate from
@@ -100,15 +136,18 @@ def keyword_leg(F, torch, dev, stream, n_launch):
     bs = torch.empty((S,), dtype=torch.int32, device=dev)
     tokens = torch.empty((T, S), dtype=torch.int32, device=dev)
 
-    def decode(lm, alpha, beta, traffic=None):
+    def reset(lm):
         ls.fill_(F.ngram_bos_state(lm))
         bs.zero_()
+
+    def decode(lm, alpha, beta, traffic=None):
         F.fusion_run(lm, gtr, x, T, S, 1, V, 1, alpha, beta, kw.blank, F.FUSION_BLANK_AM, ls, bs, None, tokens,
                      None, None, traffic, stream.cuda_stream)
 
     conds = list(CONDITIONS) + [("ngram_keyword_synth+phrase_boost", "keyword", kw.lam, kw.beta)]
     table = {}
     for name, which, alpha, beta in conds:
+        reset(glms[which or "general"])
         decode(glms[which or "general"], alpha, beta)
         torch.cuda.synchronize()
         assert F.fusion_device_status() == 0
@@ -117,28 +156,11 @@ def keyword_leg(F, torch, dev, stream, n_launch):
         table[name] = {"alpha": alpha, "beta": beta, "recall": r, "terms_found": hit, "terms": tot,
                        "token_error_rate": token_error_rate(hy, kw.refs)}
     lm = glms["keyword"]
-    traffic = torch.zeros(2, dtype=torch.int64, device=dev)
-    decode(lm, kw.lam, kw.beta, traffic)
-    torch.cuda.synchronize()
-    alg, steps = (int(v) for v in traffic.cpu())
-    for _ in range(2):
-        decode(lm, kw.lam, kw.beta)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_launch)]
-    torch.cuda.synchronize()
-    for a, b in ev:
-        ls.fill_(F.ngram_bos_state(lm))
-        bs.zero_()
-        a.record(stream)
-        F.fusion_run(lm, gtr, x, T, S, 1, V, 1, kw.lam, kw.beta, kw.blank, F.FUSION_BLANK_AM, ls, bs, None, tokens,
-                     None, None, None, stream.cuda_stream)
-        b.record(stream)
-    torch.cuda.synchronize()
-    kms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-    ach = alg / (kms / 1e3) / 1e9
-    log(f"keyword workload: {kms:.3f} ms kernel, {alg / max(steps, 1):.0f} B/hyp-step, {ach:.1f} GB/s; recall " +
-        ", ".join(f"{n} {v['recall']:.3f}" for n, v in table.items()))
-    rec = recorded_traffic(kw.name, TRAFFIC_FILE_KW)
-    ok = rec is not None and rec[1] == kernel_sources_digest()
+    alg, steps, kms = time_leg(F, torch, dev, stream, lambda: reset(lm),
+                               lambda tr: decode(lm, kw.lam, kw.beta, tr), n_launch)
+    roof = leg_roofline(alg, steps, kms, recorded_traffic(kw.name, TRAFFIC_FILE_KW))
+    log(f"keyword workload: {kms:.3f} ms kernel, {alg / max(steps, 1):.0f} B/hyp-step, {roof['achieved']:.1f} GB/s; "
+        "recall " + ", ".join(f"{n} {v['recall']:.3f}" for n, v in table.items()))
     return {
         "workload": kw.name, "streams": S, "frames": T, "V": V, "lm_order": kw.N,
         "ngrams": {k: int(sum(kw.lm(k).counts)) for k in ("general", "keyword", "refs")},
@@ -147,11 +169,7 @@ def keyword_leg(F, torch, dev, stream, n_launch):
         "timed": "ngram_keyword_synth+phrase_boost", "launches": n_launch, "kernel_ms_per_launch": kms,
         "value": float(T) * S * V / (kms / 1e3), "unit": "hyp×vocab scores/s",
         "decode_steps_per_s": T / (kms / 1e3),
-        "roofline": {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": ach / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg,
-                     "bytes_per_hyp_step": alg / max(steps, 1), "traffic": rec[0] if ok else None,
-                     "traffic_note": ("HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)"
-                                      if ok else "no PMC record for these kernel sources")},
+        "roofline": roof,
     }
 
 
@@ -343,34 +361,18 @@ def main():
         ls2_0 = torch.stack([ls0, torch.full((H,), F.ngram_bos_state(lm2), dtype=torch.int32, device=dev)])
         ls2 = ls2_0.clone()
 
-        def run2(traffic=None):
+        def reset2():
             ls2.copy_(ls2_0)
             bs.copy_(bs0)
             sc.copy_(sc0)
+
+        def run2(traffic):
             F.fusion_run_lms(lms2, alphas2, trie, x, T, S, B, V, k, w.beta, w.blank, mode, ls2, bs, sc,
                              tokens, parents if B > 1 else None, None, traffic, stream=stream.cuda_stream)
 
-        traffic2 = torch.zeros(2, dtype=torch.int64, device=dev)
-        run2(traffic2)
-        torch.cuda.synchronize()
-        assert F.fusion_device_status() == 0
-        alg2, steps2 = (int(v) for v in traffic2.cpu())
-        for _ in range(2):
-            run2()
         n2 = max(3, args.steps // 4)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n2)]
-        torch.cuda.synchronize()
-        for a, b in ev:
-            ls2.copy_(ls2_0)
-            bs.copy_(bs0)
-            sc.copy_(sc0)
-            a.record(stream)
-            F.fusion_run_lms(lms2, alphas2, trie, x, T, S, B, V, k, w.beta, w.blank, mode, ls2, bs, sc,
-                             tokens, parents if B > 1 else None, None, None, stream=stream.cuda_stream)
-            b.record(stream)
-        torch.cuda.synchronize()
-        k2 = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-        ach2 = alg2 / (k2 / 1e3) / 1e9
+        alg2, steps2, k2 = time_leg(F, torch, dev, stream, reset2, run2, n2)
+        roof2 = leg_roofline(alg2, steps2, k2, recorded_traffic(w.name + "+keyword4", TRAFFIC_FILE_TWO_LMS))
         out["two_lms"] = {
             "kernel": "fusion_kernel (two LMs)", "launches": n2, "kernel_ms_per_launch": k2,
             "value": float(T) * H * V / (k2 / 1e3), "unit": "hyp×vocab scores/s",
@@ -378,17 +380,9 @@ def main():
             "second_lm": {"kind": "keyword 4-gram (inserted phrases in Zipf carriers)",
                           "ngrams": int(sum(lm2_arrays.counts)), "ngrams_per_order": lm2_arrays.counts,
                           "lm_states": n2_states, "lm_device_bytes": lm2_bytes},
-            "roofline": {"bound": "hbm", "achieved": ach2, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": ach2 / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg2,
-                         "bytes_per_hyp_step": alg2 / max(steps2, 1)},
+            "roofline": roof2,
         }
-        rec2 = recorded_traffic(w.name + "+keyword4", TRAFFIC_FILE_TWO_LMS)
-        ok2 = rec2 is not None and rec2[1] == kernel_sources_digest()
-        out["two_lms"]["roofline"]["traffic"] = rec2[0] if ok2 else None
-        out["two_lms"]["roofline"]["traffic_note"] = (
-            "HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)" if ok2
-            else "no PMC record for these kernel sources")
-        log(f"two LMs: {k2:.3f} ms kernel, {alg2 / max(steps2, 1):.0f} B/hyp-step, {ach2:.1f} GB/s")
+        log(f"two LMs: {k2:.3f} ms kernel, {alg2 / max(steps2, 1):.0f} B/hyp-step, {roof2['achieved']:.1f} GB/s")
         del lm2
 
     # the same decode with beam recombination (candidates that reach the same
@@ -397,49 +391,25 @@ def main():
         ls1 = ls0.view(1, H)
         lsr = ls1.clone()
 
-        def run_rc(traffic=None):
+        def reset_rc():
             lsr.copy_(ls1)
             bs.copy_(bs0)
             sc.copy_(sc0)
+
+        def run_rc(traffic):
             F.fusion_run_lms([lm], [w.lam], trie, x, T, S, B, V, k, w.beta, w.blank, mode, lsr, bs, sc, tokens,
                              parents, None, traffic, flags=F.FUSION_RUN_RECOMBINE, stream=stream.cuda_stream)
 
-        traffic3 = torch.zeros(2, dtype=torch.int64, device=dev)
-        run_rc(traffic3)
-        torch.cuda.synchronize()
-        assert F.fusion_device_status() == 0
-        alg3, steps3 = (int(v) for v in traffic3.cpu())
-        for _ in range(2):
-            run_rc()
         n3 = max(3, args.steps // 4)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n3)]
-        torch.cuda.synchronize()
-        for a, b in ev:
-            lsr.copy_(ls1)
-            bs.copy_(bs0)
-            sc.copy_(sc0)
-            a.record(stream)
-            F.fusion_run_lms([lm], [w.lam], trie, x, T, S, B, V, k, w.beta, w.blank, mode, lsr, bs, sc, tokens,
-                             parents, None, None, flags=F.FUSION_RUN_RECOMBINE, stream=stream.cuda_stream)
-            b.record(stream)
-        torch.cuda.synchronize()
-        k3 = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-        ach3 = alg3 / (k3 / 1e3) / 1e9
+        alg3, steps3, k3 = time_leg(F, torch, dev, stream, reset_rc, run_rc, n3)
+        roof3 = leg_roofline(alg3, steps3, k3, recorded_traffic(w.name + "+recombine", TRAFFIC_FILE_RC))
         out["recombining_beam"] = {
             "kernel": "fusion_kernel (beam with recombination)", "launches": n3, "kernel_ms_per_launch": k3,
             "value": float(T) * H * V / (k3 / 1e3), "unit": "hyp×vocab scores/s",
             "decode_steps_per_s": T / (k3 / 1e3),
-            "roofline": {"bound": "hbm", "achieved": ach3, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": ach3 / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": alg3,
-                         "bytes_per_hyp_step": alg3 / max(steps3, 1)},
+            "roofline": roof3,
         }
-        rec3 = recorded_traffic(w.name + "+recombine", TRAFFIC_FILE_RC)
-        ok3 = rec3 is not None and rec3[1] == kernel_sources_digest()
-        out["recombining_beam"]["roofline"]["traffic"] = rec3[0] if ok3 else None
-        out["recombining_beam"]["roofline"]["traffic_note"] = (
-            "HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)" if ok3
-            else "no PMC record for these kernel sources")
-        log(f"recombining beam: {k3:.3f} ms kernel, {alg3 / max(steps3, 1):.0f} B/hyp-step, {ach3:.1f} GB/s")
+        log(f"recombining beam: {k3:.3f} ms kernel, {alg3 / max(steps3, 1):.0f} B/hyp-step, {roof3['achieved']:.1f} GB/s")
 
     if not args.no_keyword:
         out["keyword_workload"] = keyword_leg(F, torch, dev, stream, max(3, args.steps // 4))
