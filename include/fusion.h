@@ -137,7 +137,10 @@ int boost_info(const BoostTrie *t, int32_t *n_nodes, int32_t *max_depth, int64_t
 void boost_free(BoostTrie *t);
 
 /*
- * fusion_step - one decode step for H independent hypotheses.
+ * fusion_step - one decode step for H independent hypotheses: Eq. (1) of
+ * Sec. III-C over the full vocabulary of each hypothesis (the acoustic term
+ * is the log-softmax of the joint output, Sec. III), then the greedy token of
+ * Sec. III or the top-k, and the LM / phrase state after each selected token.
  *   lm, trie     handles (trie NULL: the beta term is 0)
  *   logits       device [H, V] fp32, row-major (joint output of this frame)
  *   lm_state     device [H] LM state ids;  boost_state device [H] phrase state ids
@@ -165,7 +168,12 @@ int fusion_step(const NgramTables *lm, const BoostTrie *trie, const float *logit
 
 /*
  * fusion_run - T consecutive frames for S streams of B hypotheses
- * (H = S * B, hypothesis h = s * B + b), in one launch.
+ * (H = S * B, hypothesis h = s * B + b), in one launch: the frame loop of the
+ * streaming decoder (Sec. III, greedy decoding; Sec. IV-A, 80 ms frames fed
+ * in look-ahead chunks, e.g. 13 frames for 1040 ms), each frame one
+ * fusion_step of Eq. (1) with the states carried from frame to frame.  The
+ * beam (B > 1) is not in the paper, which decodes greedily: it extends the
+ * same step to k candidates per hypothesis.
  *   logits       device [T, H, V] fp32
  *   B == 1       greedy: k must be 1; hyp_score and parents may be NULL
  *   B > 1        frame-synchronous beam (one symbol per frame): every live
@@ -210,6 +218,16 @@ int fusion_run(const NgramTables *lm, const BoostTrie *trie, const float *logits
  *                first of them in candidate order (parent asc, rank asc), whose
  *                total becomes the log-sum of theirs (fp64, folded in that
  *                order); the others leave the ranking.  Ignored for B == 1.
+ *   hist         (run) device [H] uint64 or NULL, used only with
+ *                FUSION_RUN_RECOMBINE: in, each slot's history hash carried
+ *                from the previous call of the same streams (0 at the start of
+ *                a stream: the history then begins at the slot's initial
+ *                states); out, the hash after the last frame.  Passing the same
+ *                buffer to consecutive calls makes a chunked recombining beam
+ *                equal to one call over all frames.  With NULL every call
+ *                starts each slot's history at its initial states, so slots
+ *                whose states agree at a call boundary can merge although
+ *                their earlier tokens differ.
  * Every other argument is as in fusion_step / fusion_run (beta is the boost
  * weight).  Keys are fp32 with one rounding per operation, the LM terms added
  * in the order of lms: key = (...((x + a_1 lm_1) + a_2 lm_2)...) + beta boost.
@@ -225,7 +243,8 @@ int fusion_run_lms(const NgramTables *const *lms, const float *alphas, int32_t n
                    const BoostTrie *trie, const float *logits, int32_t T, int32_t S, int32_t B,
                    int32_t V, int32_t k, float beta, int32_t blank_id, int32_t blank_mode,
                    int32_t *lm_state, int32_t *boost_state, double *hyp_score, int32_t *tokens,
-                   int32_t *parents, float *fused, int64_t *traffic, int32_t flags, hipStream_t stream);
+                   int32_t *parents, float *fused, int64_t *traffic, int32_t flags, uint64_t *hist,
+                   hipStream_t stream);
 
 /*
  * fusion_end_scores - end-of-stream scoring: the LM terms of Eq. (1) for the

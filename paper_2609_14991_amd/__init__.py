@@ -10,8 +10,11 @@ fallback.
 
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import sys
+import weakref
 
 import numpy as np
 
@@ -82,7 +85,7 @@ def lib():
                                       vp, vp, vp, vp, vp]
         L.fusion_run_lms.restype = ctypes.c_int
         L.fusion_run_lms.argtypes = [vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f32, i32, i32, vp,
-                                     vp, vp, vp, vp, vp, vp, i32, vp]
+                                     vp, vp, vp, vp, vp, vp, i32, vp, vp]
         L.fusion_end_scores.restype = ctypes.c_int
         L.fusion_end_scores.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp]
         L.joint_project.restype = ctypes.c_int
@@ -121,36 +124,60 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
-class NgramTables:
+# Device handles still alive when the interpreter begins to shut down are
+# released by an atexit hook, while the HIP runtime is certainly still up;
+# a handle's __del__ never calls into the library once shutdown has begun
+_live = weakref.WeakSet()
+
+
+def _release_all():
+    for h in list(_live):
+        h.close()
+
+
+atexit.register(_release_all)
+
+
+class _Handle:
+    _free_fn = None
+
+    def __init__(self, handle):
+        self.h = ctypes.c_void_p(handle)
+        _live.add(self)
+
+    def close(self):
+        """Release the device memory now (idempotent)."""
+        if getattr(self, "h", None) is not None and self.h.value:
+            getattr(lib(), self._free_fn)(self.h)
+        self.h = None
+
+    def __del__(self):
+        if sys.is_finalizing():
+            return
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class NgramTables(_Handle):
     """Owning handle of device-resident n-gram tables."""
 
+    _free_fn = "ngram_free"
+
     def __init__(self, handle, order, vocab, blank):
-        self.h = ctypes.c_void_p(handle)
+        super().__init__(handle)
         self.order, self.vocab, self.blank = order, vocab, blank
 
-    def __del__(self):
-        if getattr(self, "h", None) is not None and self.h.value:
-            try:
-                lib().ngram_free(self.h)
-            except Exception:  # interpreter shutdown: the module may be gone
-                pass
-            self.h = None
 
-
-class BoostTrie:
+class BoostTrie(_Handle):
     """Owning handle of a device-resident phrase-boosting tree."""
 
-    def __init__(self, handle, vocab, blank):
-        self.h = ctypes.c_void_p(handle)
-        self.vocab, self.blank = vocab, blank
+    _free_fn = "boost_free"
 
-    def __del__(self):
-        if getattr(self, "h", None) is not None and self.h.value:
-            try:
-                lib().boost_free(self.h)
-            except Exception:  # interpreter shutdown: the module may be gone
-                pass
-            self.h = None
+    def __init__(self, handle, vocab, blank):
+        super().__init__(handle)
+        self.vocab, self.blank = vocab, blank
 
 
 def ngram_load(order, vocab, blank_id, tokens, logp, backoff=None, stream=None) -> NgramTables:
@@ -256,15 +283,16 @@ def fusion_step_lms(lms, alphas, trie, logits, lm_state, boost_state, H, V, beta
 
 
 def fusion_run_lms(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
-                   boost_state, hyp_score, tokens, parents, fused=None, traffic=None, flags=0, stream=None):
+                   boost_state, hyp_score, tokens, parents, fused=None, traffic=None, flags=0, hist=None,
+                   stream=None):
     """Same arguments as the C call; lms and alphas are Python sequences,
-    tensors are CUDA (HIP) tensors (lm_state [n_lm, S*B])."""
+    tensors are CUDA (HIP) tensors (lm_state [n_lm, S*B], hist [S*B] int64)."""
     hs, al, n = _lm_arrays(lms, alphas)
     _check(lib().fusion_run_lms(ctypes.cast(hs, ctypes.c_void_p), _ptr(al), n, _h(trie), _ptr(logits),
                                 int(T), int(S), int(B), int(V), int(k), float(beta), int(blank_id),
                                 int(blank_mode), _ptr(lm_state), _ptr(boost_state), _ptr(hyp_score),
                                 _ptr(tokens), _ptr(parents), _ptr(fused), _ptr(traffic), int(flags),
-                                _stream(stream)))
+                                _ptr(hist), _stream(stream)))
 
 
 def fusion_end_scores(lms, alphas, lm_state, H, hyp_score=None, end_term=None, stream=None):
@@ -358,9 +386,10 @@ def step_lms(lms, alphas, trie, logits, lm_state, boost_state, beta, blank_id, k
 
 
 def run_lms(lms, alphas, trie, logits, S, B, k, beta, blank_id, blank_mode, lm_state, boost_state,
-            hyp_score=None, want_fused=False, traffic=None, recombine=False, stream=None):
+            hyp_score=None, want_fused=False, traffic=None, recombine=False, hist=None, stream=None):
     """``run`` with several LMs: lm_state [n_lm, S*B] is updated in place;
-    ``recombine`` merges beam candidates that reach the same history."""
+    ``recombine`` merges beam candidates that reach the same history (``hist``,
+    an int64 [S*B] tensor or None, carries the history hashes across calls)."""
     import torch
 
     T, H, V = logits.shape
@@ -370,5 +399,5 @@ def run_lms(lms, alphas, trie, logits, S, B, k, beta, blank_id, blank_mode, lm_s
     fused = torch.zeros((T, H, V), dtype=torch.float32, device=dev) if want_fused else None
     fusion_run_lms(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
                    boost_state, hyp_score, tokens, parents, fused, traffic,
-                   FUSION_RUN_RECOMBINE if recombine else 0, stream)
+                   FUSION_RUN_RECOMBINE if recombine else 0, hist, stream)
     return dict(tokens=tokens, parents=parents, fused=fused)

@@ -77,6 +77,7 @@ struct Params {
   int32_t *next_lm;
   int32_t *next_boost;
   unsigned long long *xchg;  // beam exchange [S][2][B][k] candidate records of four tagged words
+  unsigned long long *hist;  // recombination: [H] in/out history hashes (0: derive from the initial states) or NULL
   int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, n_lm, recombine, pad;
   float lam[FUSION_MAX_LMS], beta;
 };
@@ -355,11 +356,17 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     hs.cur_q = q;
     hs.S = sc;
     if constexpr (RC) {
-      // the history starts at the slot's initial states
-      unsigned long long hh = mix64(0x243F6A8885A308D3ull ^ (unsigned long long)(unsigned)q);
+      // the history carried from an earlier call, else one that starts at the
+      // slot's initial states (never 0, which marks the start of a stream)
+      unsigned long long hh = p.hist ? (p.hist[h] & ((1ull << 48) - 1)) : 0ull;
+      if (hh == 0ull) {
+        hh = mix64(0x243F6A8885A308D3ull ^ (unsigned long long)(unsigned)q);
 #pragma unroll
-      for (int i = 0; i < NL; ++i) hh = mix64(hh ^ ((unsigned long long)(unsigned)hs.lmsrc[i] << (8 * i + 1)));
-      hs.hist = hh & ((1ull << 48) - 1);
+        for (int i = 0; i < NL; ++i) hh = mix64(hh ^ ((unsigned long long)(unsigned)hs.lmsrc[i] << (8 * i + 1)));
+        hh &= (1ull << 48) - 1;
+        hh = hh ? hh : 1ull;
+      }
+      hs.hist = hh;
     }
     if (alive && !(ok_lm && ok_q))
       atomicOr(&g_status, (ok_lm ? 0 : FUSION_STATUS_BAD_LM_STATE) | (ok_q ? 0 : FUSION_STATUS_BAD_BOOST_STATE));
@@ -1126,11 +1133,11 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           if constexpr (NL > 1)
             w[4] = (unsigned long long)(unsigned)cl[1] | ((unsigned long long)((hs.c1[1] + 1) & 0xFFFF) << 32) | tag;
           if constexpr (RC) {
-            // the history after the candidate: blank emits nothing
+            // the history after the candidate: blank emits nothing (a hash is
+            // never 0, which marks the start of a stream in the carried buffer)
             const unsigned long long hist = hs.hist;
-            w[XW - 1] = ((!has || cy == blank) ? hist
-                                                : (mix64(hist ^ (0x632BE59BD9B4E019ull * (unsigned long long)(cy + 1))) & kPay)) |
-                        tag;
+            const unsigned long long hn = mix64(hist ^ (0x632BE59BD9B4E019ull * (unsigned long long)(cy + 1))) & kPay;
+            w[XW - 1] = ((!has || cy == blank) ? hist : (hn ? hn : 1ull)) | tag;
           }
 #pragma unroll
           for (int q = 0; q < XW; ++q)
@@ -1319,6 +1326,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     if (moved && nq < 0) nq = tr.root_node[y].w;
     if (p.has_trie) p.boost_state[h] = nq;
     if (BEAM) p.hyp_score[h] = hs.S;
+    if constexpr (RC) {
+      if (p.hist) p.hist[h] = hs.hist;
+    }
   }
   if (p.traffic && g == 0) {
     const unsigned long long extra = (h == 0 && p.has_trie) ? 4ull * p.V * (unsigned long long)p.T : 0ull;
@@ -1540,7 +1550,8 @@ int step_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, 
 int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, const BoostTrie *trie,
              const float *logits, int32_t T, int32_t S, int32_t B, int32_t V, int32_t k, float beta,
              int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state, double *hyp_score,
-             int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, int32_t flags, hipStream_t stream) {
+             int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, int32_t flags, uint64_t *hist,
+             hipStream_t stream) {
   int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta, T != 0 && S != 0);
   if (rc != FUSION_OK) return rc;
   if (T < 0 || S < 0 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
@@ -1570,6 +1581,7 @@ int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, c
   p.step_mode = 0;
   p.beta = beta;
   p.recombine = (flags & FUSION_RUN_RECOMBINE) && B > 1;
+  p.hist = p.recombine ? reinterpret_cast<unsigned long long *>(hist) : nullptr;
   return launch(p, S * B, stream);
 }
 
@@ -1621,7 +1633,7 @@ extern "C" int fusion_run(const NgramTables *lm, const BoostTrie *trie, const fl
                           double *hyp_score, int32_t *tokens, int32_t *parents, float *fused,
                           int64_t *traffic, hipStream_t stream) {
   return run_impl(&lm, &lambda, 1, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
-                  boost_state, hyp_score, tokens, parents, fused, traffic, 0, stream);
+                  boost_state, hyp_score, tokens, parents, fused, traffic, 0, nullptr, stream);
 }
 
 extern "C" int fusion_run_lms(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
@@ -1629,7 +1641,7 @@ extern "C" int fusion_run_lms(const NgramTables *const *lms, const float *alphas
                               int32_t V, int32_t k, float beta, int32_t blank_id, int32_t blank_mode,
                               int32_t *lm_state, int32_t *boost_state, double *hyp_score, int32_t *tokens,
                               int32_t *parents, float *fused, int64_t *traffic, int32_t flags,
-                              hipStream_t stream) {
+                              uint64_t *hist, hipStream_t stream) {
   return run_impl(lms, alphas, n_lm, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
-                  boost_state, hyp_score, tokens, parents, fused, traffic, flags, stream);
+                  boost_state, hyp_score, tokens, parents, fused, traffic, flags, hist, stream);
 }

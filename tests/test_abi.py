@@ -137,5 +137,5 @@ def test_several_lm_calls_reject_bad_arguments(lib):
     assert rc == F.FUSION_E_ARG
     rc = lib.fusion_run_lms(ctypes.cast(hs, ctypes.c_void_p), ctypes.cast(al, ctypes.c_void_p), 2, None,
                             None, 1, 1, 1, 4, 1, 0.5, 0, 0, None, None, None, None, None, None, None,
-                            0, None)
+                            0, None, None)
     assert rc == F.FUSION_E_ARG and "NULL" in F.fusion_last_error()

@@ -5,8 +5,10 @@ Greedy decodes (C3) must match the oracle's own free-running decode token for
 token.  Beam decodes (C4, C5) are replayed by the oracle on the GPU's choices
 (teacher forcing): at every frame the oracle ranks the candidates itself and
 reports the first frame where its choice differs from the GPU's unless the
-two are within 1e-4 in fp64 score (a near tie, accepted and counted).  Final
-LM / phrase states must be equal and final beam scores within 1e-5 per frame.
+two are within 1e-4 in fp64 score (a near tie, accepted and counted).  These
+workloads have no near ties: every decision must be the oracle's own (the
+count is asserted to be 0).  Final LM / phrase states must be equal and final
+beam scores within 1e-5 per frame.
 
 Estimating the C4 model (20M sentences) takes about a minute on the host.
 """
@@ -59,6 +61,7 @@ def beam_vs_oracle(w, label):
                    forced_tokens=tok, forced_parents=par, tol=TIE_TOL, threads=threads())
     bad = np.nonzero(r["mismatch_at"] >= 0)[0]
     assert bad.size == 0, f"{label}: streams {bad[:5]} diverge at frames {r['mismatch_at'][bad[:5]]}"
+    assert int(r["near_ties"].sum()) == 0, f"{label}: {int(r['near_ties'].sum())} near ties"
     assert np.array_equal(ls.cpu().numpy(), r["lm_state"]), f"{label}: final LM states"
     assert np.array_equal(bs.cpu().numpy(), r["boost_state"]), f"{label}: final phrase states"
     got, ref = sc.cpu().numpy(), r["hyp_score"]
@@ -162,6 +165,7 @@ def test_c5_two_lms_full_beam():
                        forced_parents=out["parents"].cpu().numpy(), tol=TIE_TOL, threads=threads())
     bad = np.nonzero(r["mismatch_at"] >= 0)[0]
     assert bad.size == 0, f"streams {bad[:5]} diverge at frames {r['mismatch_at'][bad[:5]]}"
+    assert int(r["near_ties"].sum()) == 0, f"{int(r['near_ties'].sum())} near ties"
     assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
     assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
     fin = np.isfinite(r["hyp_score"])
@@ -192,6 +196,7 @@ def test_c5_recombining_beam():
                        tol=TIE_TOL, threads=threads(), recombine=True)
     bad = np.nonzero(r["mismatch_at"] >= 0)[0]
     assert bad.size == 0, f"streams {bad[:5]} diverge at frames {r['mismatch_at'][bad[:5]]}"
+    assert int(r["near_ties"].sum()) == 0, f"{int(r['near_ties'].sum())} near ties"
     assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
     assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
     fin = np.isfinite(r["hyp_score"])

@@ -302,3 +302,41 @@ def test_recombining_beam_teacher_forced(n_lm):
     r0 = oracle.run_lms([oracle.OracleLM(m) for m in lms], alphas, oracle.OracleTrie(V, 0, ph), x, S, B, k, 0.5,
                         0, 1, [[V] * H] * n_lm, [0] * H, sc0, threads=8)
     assert not np.array_equal(r0["hyp_score"], r["hyp_score"])
+
+
+def test_recombining_beam_chunked_equals_one_call():
+    """A recombining beam decoded in 13-frame chunks, with the states, scores
+    and history hashes carried from call to call (the streaming use of
+    Sec. IV-A), gives exactly the tokens, parents, states and scores of one
+    call over all frames; the one call is the oracle-checked decode above."""
+    rng = np.random.default_rng(97)
+    V, S, B, k, T = 300, 24, 4, 4, 40
+    lm = tiny_random_lm(rng, V, 4, n_sent=3000)
+    ph = tiny_random_phrases(rng, V, n=40, max_len=4, alphabet=30, with_completion=True)
+    glm, gtr = F.ngram_load_arrays(lm), F.boost_build_phrases(V, 0, ph)
+    H = S * B
+    x = (rng.standard_normal((T, H, V)) * 2).astype(np.float32)
+    x[:, :, 0] += 3
+    xd = torch.from_numpy(x).to(dev())
+    sc0 = torch.from_numpy(np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)).to(dev())
+
+    def fresh():
+        return (torch.full((1, H), V, dtype=torch.int32, device=dev()), torch.zeros((H,), dtype=torch.int32, device=dev()),
+                sc0.clone(), torch.zeros((H,), dtype=torch.int64, device=dev()))
+
+    ls, bs, sc, hh = fresh()
+    one = F.run_lms([glm], [0.5], gtr, xd, S, B, k, 0.5, 0, F.FUSION_BLANK_COMPETE, ls, bs, sc, recombine=True, hist=hh)
+    ls2, bs2, sc2, hh2 = fresh()
+    toks, pars = [], []
+    for t0 in range(0, T, 13):
+        o = F.run_lms([glm], [0.5], gtr, xd[t0:t0 + 13].contiguous(), S, B, k, 0.5, 0, F.FUSION_BLANK_COMPETE,
+                      ls2, bs2, sc2, recombine=True, hist=hh2)
+        toks.append(o["tokens"])
+        pars.append(o["parents"])
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    assert torch.equal(torch.cat(toks), one["tokens"])
+    assert torch.equal(torch.cat(pars), one["parents"])
+    assert torch.equal(ls2, ls) and torch.equal(bs2, bs) and torch.equal(hh2, hh)
+    assert torch.equal(sc2, sc)
+    assert bool((hh != 0).all())
