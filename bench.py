@@ -7,11 +7,15 @@ beam merge (every step of the path, inputs resident in HBM).
 
 Prints one JSON line: hyp x vocab scores/s (value), decode steps/s, the
 roofline of the fusion kernel (algorithmic bytes per launch / mean launch
-time from HIP events) and the CPU oracle timed on a bounded sample of the
-same workload, whose decisions are also checked against the GPU trajectory.
-Beside the main step it times the joint output projection, the decode with a
+time from HIP events), and the CPU oracle timed on bounded samples of the
+same workload (all host cores the run may use, and one thread), whose
+decisions are also checked against the GPU trajectory.  Beside the main step
+it reports, each in its own object: the other four workloads (C1-C4, C2 as
+its 77 chunk calls), a single fusion_step call on C5 timed with its launch,
+C5 with the fused rows written, a measured device-copy bandwidth, the joint
+output projection (per frame and batched over all frames), the decode with a
 second LM, the recombining beam and the keyword workload (the steering
-conditions of Table II on synthetic terms and logits), each in its own object.
+conditions of Table II on synthetic terms and logits).
 """
 
 from __future__ import annotations
@@ -32,6 +36,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, vendor figure
 METRIC = "fused hyp×vocab scores/sec + decode steps/sec; achieved HBM GB/s vs peak"
+HOST_THREADS_CAP = 16  # the host-CPU share of one GPU on the measurement machines
 
 
 def log(msg):
@@ -68,6 +73,16 @@ def recorded_traffic(workload, path=None):
     return int(float(fields["traffic_bytes_per_launch"])), fields.get("kernel_sources_digest")
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def copy_probe(nbytes):
     """A plain device copy of known size, for scaling the FETCH_SIZE / WRITE_SIZE counters."""
     import torch
@@ -80,6 +95,26 @@ def copy_probe(nbytes):
         dst.copy_(src)
     torch.cuda.synchronize()
     log(f"copied {n * 4} bytes 3 times")
+
+
+def copy_bandwidth(torch, stream, nbytes=1 << 31, reps=10):
+    """Measured device-to-device copy rate (bytes read + bytes written per second)."""
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    del src, dst
+    return {"bytes_per_copy": nbytes, "ms": ms, "gbs": 2.0 * nbytes / (ms / 1e3) / 1e9,
+            "note": "torch device copy of 2 GiB fp32: bytes read + bytes written per second"}
 
 
 def time_leg(F, torch, dev, stream, reset, launch, n_launch):
@@ -107,15 +142,70 @@ def time_leg(F, torch, dev, stream, reset, launch, n_launch):
     return alg, steps, float(np.mean([a.elapsed_time(b) for a, b in ev]))
 
 
-def leg_roofline(alg, steps, kms, record):
+def leg_roofline(alg, steps, kms, record, copy_gbs=None):
     """The roofline object of a leg; `record` is its PMC traffic record or None."""
     ach = alg / (kms / 1e3) / 1e9
     ok = record is not None and record[1] == kernel_sources_digest()
-    return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
-            "algorithmic_bytes_per_launch": alg, "bytes_per_hyp_step": alg / max(steps, 1),
-            "traffic": record[0] if ok else None,
-            "traffic_note": ("HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)" if ok
-                             else "no PMC record for these kernel sources")}
+    out = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+           "algorithmic_bytes_per_launch": alg, "bytes_per_hyp_step": alg / max(steps, 1),
+           "traffic": record[0] if ok else None,
+           "traffic_note": ("HBM bytes per launch from the PMC record (FETCH_SIZE + WRITE_SIZE, scaled)" if ok
+                            else "no PMC record for these kernel sources")}
+    if ok:
+        out["hbm_traffic_gbs"] = record[0] / (kms / 1e3) / 1e9
+    if copy_gbs:
+        out["frac_of_copy"] = ach / copy_gbs
+    return out
+
+
+def config_leg(F, torch, dev, stream, cfg, n_launch, copy_gbs):
+    """Workload cfg (1-4) decoded on the GPU as the tests check it: µs per
+    decode step (frame), decode steps/s, hyp x vocab scores/s and its roofline.
+    C2 is its 1000 frames fed as 77 calls of 13 frames (the last of 12) with
+    the states carried, timed as the sum of the calls."""
+    from workloads import load_workload
+
+    t0 = time.time()
+    w = load_workload(cfg)
+    lm = F.ngram_load_arrays(w.lm)
+    trie = F.boost_build_phrases(w.V, w.blank, w.phrases)
+    T, S, B, V, k, H = w.T, w.S, w.B, w.V, w.k, w.H
+    x = torch.from_numpy(w.logits).to(dev)
+    bos = F.ngram_bos_state(lm)
+    ls = torch.full((H,), bos, dtype=torch.int32, device=dev)
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev)
+    sc0 = torch.from_numpy(np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)).to(dev)
+    sc = sc0.clone()
+    tokens = torch.empty((T, H), dtype=torch.int32, device=dev)
+    parents = torch.empty((T, H), dtype=torch.int32, device=dev) if B > 1 else None
+    mode = F.FUSION_BLANK_COMPETE if B > 1 else F.FUSION_BLANK_AM
+    chunk = w.chunk if w.chunk else T
+    log(f"{w.name}: built in {time.time() - t0:.1f}s")
+
+    def reset():
+        ls.fill_(bos)
+        bs.zero_()
+        sc.copy_(sc0)
+
+    def launch(traffic):
+        for t0_ in range(0, T, chunk):
+            t1_ = min(T, t0_ + chunk)
+            F.fusion_run(lm, trie, x[t0_:t1_], t1_ - t0_, S, B, V, k, w.lam, w.beta, w.blank, mode, ls, bs,
+                         sc if B > 1 else None, tokens[t0_:t1_], parents[t0_:t1_] if B > 1 else None, None,
+                         traffic, stream.cuda_stream)
+
+    alg, steps, kms = time_leg(F, torch, dev, stream, reset, launch, n_launch)
+    roof = leg_roofline(alg, steps, kms, None, copy_gbs)
+    calls = (T + chunk - 1) // chunk
+    out = {"workload": w.name, "V": V, "lm_order": w.N, "ngrams": int(sum(w.lm.counts)), "phrases": w.phrases.n,
+           "streams": S, "beam": B, "hypotheses": H, "frames": T, "k": k, "calls": calls,
+           "ms_per_run": kms, "us_per_step": kms * 1e3 / T, "decode_steps_per_s": T / (kms / 1e3),
+           "value": float(T) * H * V / (kms / 1e3), "unit": "hyp×vocab scores/s", "roofline": roof}
+    log(f"{w.name}: {kms:.3f} ms for {T} frames in {calls} call(s), {kms * 1e3 / T:.2f} us/step, "
+        f"{alg / max(steps, 1):.0f} B/hyp-step, frac {roof['frac']:.4f}")
+    lm.close()
+    trie.close()
+    return out
 
 
 def keyword_leg(F, torch, dev, stream, n_launch):
@@ -161,6 +251,8 @@ def keyword_leg(F, torch, dev, stream, n_launch):
     roof = leg_roofline(alg, steps, kms, recorded_traffic(kw.name, TRAFFIC_FILE_KW))
     log(f"keyword workload: {kms:.3f} ms kernel, {alg / max(steps, 1):.0f} B/hyp-step, {roof['achieved']:.1f} GB/s; "
         "recall " + ", ".join(f"{n} {v['recall']:.3f}" for n, v in table.items()))
+    for h in list(glms.values()) + [gtr]:
+        h.close()
     return {
         "workload": kw.name, "streams": S, "frames": T, "V": V, "lm_order": kw.N,
         "ngrams": {k: int(sum(kw.lm(k).counts)) for k in ("general", "keyword", "refs")},
@@ -173,13 +265,115 @@ def keyword_leg(F, torch, dev, stream, n_launch):
     }
 
 
+def projection_leg(F, torch, dev, stream, cfg):
+    """The joint output projection (bf16 MFMA) that would produce C5's logits:
+    the per-frame shape [256, 640] x [640, 4096] (one frame of all hypotheses)
+    and the batch of all 300 frames [76800, 640] x [640, 4096], each timed with
+    HIP events over back-to-back launches."""
+    from workloads import make_projection
+
+    A, Wt, bias = make_projection(cfg)
+    M, K = A.shape
+    N = Wt.shape[0]
+    a_d = torch.from_numpy(A.view(np.int16)).to(dev)
+    w_d = torch.from_numpy(Wt.view(np.int16)).to(dev)
+    b_d = torch.from_numpy(bias).to(dev)
+    o_d = torch.empty((M, N), dtype=torch.float32, device=dev)
+    out = {"kernel": "joint_proj_kernel"}
+    H = M // 300
+    for name, m, n_rep in (("per_frame", H, 200), ("batched", M, 10)):
+        for _ in range(3):
+            F.joint_project(a_d, w_d, b_d, m, N, K, o_d, stream.cuda_stream)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n_rep):
+            F.joint_project(a_d, w_d, b_d, m, N, K, o_d, stream.cuda_stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        pms = e0.elapsed_time(e1) / n_rep
+        flops = 2.0 * m * N * K
+        pbytes = 2.0 * m * K + 2.0 * N * K + 4.0 * N + 4.0 * m * N
+        out[name] = {
+            "shape": [m, N, K], "ms_per_launch": pms, "launches": n_rep,
+            "tflops": flops / (pms / 1e3) / 1e12, "peak_tflops_bf16": BF16_PEAK_TFLOPS,
+            "frac_of_peak": flops / (pms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
+            "min_hbm_bytes": pbytes, "hbm_gbs_at_min_bytes": pbytes / (pms / 1e3) / 1e9,
+        }
+        log(f"joint projection {m}x{N}x{K}: {pms * 1e3:.1f} us, {flops / (pms / 1e3) / 1e12:.1f} TFLOP/s")
+    del a_d, w_d, b_d, o_d
+    return out
+
+
+def step_leg(F, torch, dev, stream, w, lm, trie, x, n_calls=300):
+    """One fusion_step over C5's 256 hypotheses at a frame of its decode: the
+    host-side time per call including its launch (calls back to back, one
+    synchronisation at the end), and the HIP-event time of one call."""
+    H, V = w.H, w.V
+    rng = np.random.default_rng(5)
+    ls = torch.from_numpy(rng.integers(1, V, size=H).astype(np.int32)).to(dev)
+    bs = torch.zeros((H,), dtype=torch.int32, device=dev)
+    out = {n: torch.empty((H, w.k), dtype=dt, device=dev)
+           for n, dt in (("tokens", torch.int32), ("scores", torch.float32), ("next_lm", torch.int32),
+                         ("next_boost", torch.int32))}
+    row = x[w.T // 2]
+
+    def call():
+        F.fusion_step(lm, trie, row, ls, bs, H, V, w.lam, w.beta, w.blank, w.k, F.FUSION_BLANK_COMPETE, None,
+                      out["tokens"], out["scores"], out["next_lm"], out["next_boost"], stream.cuda_stream)
+
+    for _ in range(10):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(n_calls):
+        call()
+    torch.cuda.synchronize()
+    host_us = (time.perf_counter() - t0) / n_calls * 1e6
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(50)]
+    for a, b in ev:
+        a.record(stream)
+        call()
+        b.record(stream)
+    torch.cuda.synchronize()
+    ev_us = float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+    assert F.fusion_device_status() == 0
+    log(f"fusion_step (C5, 256 hypotheses, top-4): {host_us:.2f} us per call with launch, {ev_us:.2f} us events")
+    return {"hypotheses": H, "V": V, "k": w.k, "calls": n_calls, "us_per_call_launch_inclusive": host_us,
+            "us_per_call_events": ev_us, "note": "random one-token LM states, root phrase state; states not "
+            "advanced between calls"}
+
+
+def cpu_leg(w, ref_tokens, ref_parents, bos, n_threads, streams, frames):
+    """The oracle on the first `frames` frames of `streams` streams of the
+    workload, replaying the GPU's decisions, on n_threads threads."""
+    import oracle
+
+    olm = oracle.OracleLM(w.lm)
+    otr = oracle.OracleTrie(w.V, w.blank, w.phrases)
+    B, k, V = w.B, w.k, w.V
+    Sc, Tc = min(streams, w.S), min(frames, w.T)
+    xs = np.ascontiguousarray(w.logits[:Tc, :Sc * B])
+    sc_init = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), Sc)
+    tc = time.perf_counter()
+    r = oracle.run(olm, otr, xs, Sc, B, k, w.lam, w.beta, w.blank, 1 if B > 1 else 0,
+                   [bos] * (Sc * B), [0] * (Sc * B), sc_init,
+                   forced_tokens=ref_tokens[:Tc, :Sc * B],
+                   forced_parents=ref_parents[:Tc, :Sc * B] if B > 1 else None,
+                   tol=1e-4, threads=n_threads)
+    sec = time.perf_counter() - tc
+    agree = bool((r["mismatch_at"] < 0).all())
+    near = int(r["near_ties"].sum())
+    return olm, otr, r, sec, Sc, Tc, agree, near
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=5)
-    ap.add_argument("--fused", action="store_true", help="also write the full fused score rows")
+    ap.add_argument("--fused", action="store_true", help="time the main step with the full fused score rows written")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-projection", action="store_true", help="skip the joint-projection measurement")
     ap.add_argument("--no-recombine", action="store_true", help="skip the recombining-beam measurement")
@@ -187,8 +381,11 @@ def main():
                     help="skip the two-LM measurement (C5 with a second, keyword 4-gram LM)")
     ap.add_argument("--no-keyword", action="store_true",
                     help="skip the keyword workload (steering conditions of Table II, synthetic)")
+    ap.add_argument("--no-configs", action="store_true", help="skip the C1-C4 rows")
     ap.add_argument("--cpu-frames", type=int, default=300)
     ap.add_argument("--cpu-streams", type=int, default=64)
+    ap.add_argument("--cpu-streams-single", type=int, default=4,
+                    help="streams of the single-thread oracle sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of this size (counter calibration) and exit")
     args = ap.parse_args()
@@ -208,6 +405,7 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
     t0 = time.time()
     w = load_workload(args.config)
     log(f"workload {w.name}: n-grams {w.lm.counts} built in {time.time() - t0:.1f}s")
@@ -231,18 +429,20 @@ def main():
     parents = torch.empty((T, H), dtype=torch.int32, device=dev)
     fused = torch.empty((T, H, V), dtype=torch.float32, device=dev) if args.fused else None
     mode = F.FUSION_BLANK_COMPETE if B > 1 else F.FUSION_BLANK_AM
-    stream = torch.cuda.current_stream()
 
-    def one_step(traffic=None):
+    def reset():
         ls.copy_(ls0)
         bs.copy_(bs0)
         sc.copy_(sc0)
+
+    def run_once(traffic=None, fused_rows=fused):
         F.fusion_run(lm, trie, x, T, S, B, V, k, w.lam, w.beta, w.blank, mode, ls, bs, sc, tokens,
-                     parents if B > 1 else None, fused, traffic, stream.cuda_stream)
+                     parents if B > 1 else None, fused_rows, traffic, stream.cuda_stream)
 
     # algorithmic bytes of one launch (visited states), counted by the kernel
     traffic = torch.zeros(2, dtype=torch.int64, device=dev)
-    one_step(traffic)
+    reset()
+    run_once(traffic)
     torch.cuda.synchronize()
     alg_bytes, hyp_steps = (int(v) for v in traffic.cpu())
     ref_tokens = tokens.cpu().numpy().copy()
@@ -250,19 +450,17 @@ def main():
     assert F.fusion_device_status() == 0
 
     for _ in range(args.warmup):
-        one_step()
+        reset()
+        run_once()
     torch.cuda.synchronize()
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     torch.cuda.synchronize()
     tw = time.perf_counter()
     for i in range(args.steps):
-        ls.copy_(ls0)
-        bs.copy_(bs0)
-        sc.copy_(sc0)
+        reset()
         starts[i].record(stream)
-        F.fusion_run(lm, trie, x, T, S, B, V, k, w.lam, w.beta, w.blank, mode, ls, bs, sc, tokens,
-                     parents if B > 1 else None, fused, None, stream.cuda_stream)
+        run_once()
         ends[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - tw
@@ -272,9 +470,11 @@ def main():
     scores = float(T) * H * V
     value = scores / (ms_per_step / 1e3)
     achieved = alg_bytes / (kern_ms / 1e3) / 1e9
-    log(f"fusion_run: {ms_per_step:.3f} ms/step wall, {kern_ms:.3f} ms kernel, "
+    log(f"fusion_run: {ms_per_step:.3f} ms/step wall, {kern_ms:.3f} ms kernel, {kern_ms * 1e3 / T:.2f} us/frame, "
         f"{alg_bytes / hyp_steps:.0f} B/hyp-step, {achieved:.1f} GB/s")
 
+    copy = copy_bandwidth(torch, stream)
+    log(f"device copy: {copy['gbs']:.0f} GB/s")
     out = {
         "metric": METRIC,
         "value": value,
@@ -295,8 +495,12 @@ def main():
             "hypotheses": H, "frames": T, "k": k, "lambda": w.lam, "beta": w.beta,
             "fused_rows_written": bool(args.fused),
         },
-        "decode_steps_per_s": T / (ms_per_step / 1e3),
-        "kernel_ms_per_launch": kern_ms,
+        "step_unit": "one fusion_run launch: all 300 frames of the 256 hypotheses (ms_per_step); "
+                     "one decode step is one frame (us_per_frame)",
+        "ms_per_launch_kernel": kern_ms,
+        "us_per_frame": kern_ms * 1e3 / T,
+        "decode_steps_per_s": T / (kern_ms / 1e3),
+        "decode_steps_per_s_wall": T / (ms_per_step / 1e3),
         "table_build_s": t_load,
         "roofline": {
             "bound": "hbm",
@@ -307,45 +511,33 @@ def main():
             "traffic": None,
             "traffic_note": None,
             "algorithmic_bytes_per_launch": alg_bytes,
+            "algorithmic_bytes_source": "kernel counter over the visited states (checked against an independent "
+                                        "count in the tests and in cpu_baseline)",
             "bytes_per_hyp_step": alg_bytes / max(hyp_steps, 1),
             "hyp_steps_per_launch": hyp_steps,
             "kernel": "fusion_kernel",
+            "copy_gbs": copy["gbs"],
+            "frac_of_copy": achieved / copy["gbs"],
         },
+        "copy_bandwidth": copy,
         "cpu_baseline": None,
     }
-    # the joint output projection (bf16 MFMA) that would produce this run's logits:
-    # [T*H, 640] x [640, V], timed on its own; not part of the step above
-    if not args.no_projection:
-        from workloads import make_projection
 
-        A, Wt, bias = make_projection(args.config)
-        M, K = A.shape
-        N = Wt.shape[0]
-        a_d = torch.from_numpy(A.view(np.int16)).to(dev)
-        w_d = torch.from_numpy(Wt.view(np.int16)).to(dev)
-        b_d = torch.from_numpy(bias).to(dev)
-        o_d = torch.empty((M, N), dtype=torch.float32, device=dev)
-        for _ in range(3):
-            F.joint_project(a_d, w_d, b_d, M, N, K, o_d, stream.cuda_stream)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        n_rep = 10
-        e0.record(stream)
-        for _ in range(n_rep):
-            F.joint_project(a_d, w_d, b_d, M, N, K, o_d, stream.cuda_stream)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        pms = e0.elapsed_time(e1) / n_rep
-        flops = 2.0 * M * N * K
-        pbytes = 2.0 * M * K + 2.0 * N * K + 4.0 * N + 4.0 * M * N
-        out["projection"] = {
-            "kernel": "joint_proj_kernel", "shape": [M, N, K], "ms_per_launch": pms,
-            "tflops": flops / (pms / 1e3) / 1e12, "peak_tflops_bf16": BF16_PEAK_TFLOPS,
-            "frac_of_peak": flops / (pms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
-            "min_hbm_bytes": pbytes, "hbm_gbs_at_min_bytes": pbytes / (pms / 1e3) / 1e9,
-        }
-        log(f"joint projection {M}x{N}x{K}: {pms:.3f} ms, {flops / (pms / 1e3) / 1e12:.1f} TFLOP/s")
-        del a_d, w_d, b_d, o_d
+    # C5 with the full fused rows written (full-score mode), beside select-only
+    if not args.fused:
+        fz = torch.empty((T, H, V), dtype=torch.float32, device=dev)
+        alg_f, steps_f, kms_f = time_leg(F, torch, dev, stream, reset, lambda tr: run_once(tr, fz),
+                                         max(3, args.steps // 4))
+        out["full_score"] = {"kernel": "fusion_kernel (fused rows written)", "kernel_ms_per_launch": kms_f,
+                             "us_per_frame": kms_f * 1e3 / T, "value": scores / (kms_f / 1e3),
+                             "unit": "hyp×vocab scores/s",
+                             "roofline": leg_roofline(alg_f, steps_f, kms_f, None, copy["gbs"])}
+        log(f"full-score mode: {kms_f:.3f} ms kernel, frac {alg_f / (kms_f / 1e3) / 1e9 / HBM_PEAK_GBS:.4f}")
+        del fz
+    out["fusion_step"] = step_leg(F, torch, dev, stream, w, lm, trie, x)
+
+    if not args.no_projection:
+        out["projection"] = projection_leg(F, torch, dev, stream, args.config)
 
     # Eq. (1) with two LMs: the same decode with a second, keyword 4-gram LM
     # (weights lambda, lambda), timed the same way; not part of the step above
@@ -383,7 +575,7 @@ def main():
             "roofline": roof2,
         }
         log(f"two LMs: {k2:.3f} ms kernel, {alg2 / max(steps2, 1):.0f} B/hyp-step, {roof2['achieved']:.1f} GB/s")
-        del lm2
+        lm2.close()
 
     # the same decode with beam recombination (candidates that reach the same
     # history merge, log-summed): the kernel's recombining beam variant
@@ -424,38 +616,58 @@ def main():
         out["roofline"]["traffic_note"] = "PMC record is for the run without fused rows"
     else:
         out["roofline"]["traffic"] = rec[0]
+        out["roofline"]["hbm_traffic_gbs"] = rec[0] / (kern_ms / 1e3) / 1e9
         out["roofline"]["traffic_note"] = ("HBM bytes per launch: rocprofv3 FETCH_SIZE + WRITE_SIZE, each scaled "
-                                           "by the counter's reading for a plain copy of known size")
+                                           "by the counter's reading for a plain copy of known size; "
+                                           "hbm_traffic_gbs is that over the kernel time")
+
+    # the main step's tables are released before the other workloads are built
+    lm.close()
+    trie.close()
+    del x, tokens, parents, fused, ls, bs, sc, ls0, bs0, sc0
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    if not args.no_configs:
+        out["configs"] = {}
+        for cfg in (1, 2, 3, 4):
+            if cfg == args.config:
+                continue
+            out["configs"][f"c{cfg}"] = config_leg(F, torch, dev, stream, cfg, 5, copy["gbs"])
+            torch.cuda.empty_cache()
 
     if not args.no_cpu:
-        import oracle
+        from oracle import traffic as checker
 
-        n_thr = len(os.sched_getaffinity(0))
-        n_thr = min(n_thr, 16)
-        Sc = min(args.cpu_streams, S)
-        Tc = min(args.cpu_frames, T)
-        t2 = time.time()
-        olm = oracle.OracleLM(w.lm)
-        otr = oracle.OracleTrie(w.V, w.blank, w.phrases)
-        log(f"oracle tables loaded in {time.time() - t2:.1f}s; sample {Sc} streams x {Tc} frames on {n_thr} threads")
-        xs = np.ascontiguousarray(w.logits[:Tc, :Sc * B])
-        sc_init = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), Sc)
-        tc = time.perf_counter()
-        r = oracle.run(olm, otr, xs, Sc, B, k, w.lam, w.beta, w.blank, 1 if B > 1 else 0,
-                       [bos] * (Sc * B), [0] * (Sc * B), sc_init,
-                       forced_tokens=ref_tokens[:Tc, :Sc * B],
-                       forced_parents=ref_parents[:Tc, :Sc * B] if B > 1 else None,
-                       tol=1e-4, threads=n_thr)
-        cpu_s = time.perf_counter() - tc
-        agree = bool((r["mismatch_at"] < 0).all())
-        cpu_scores = float(Tc) * Sc * B * V / cpu_s
+        n_thr = min(len(os.sched_getaffinity(0)), HOST_THREADS_CAP)
+        olm, otr, r, sec, Sc, Tc, agree, near = cpu_leg(w, ref_tokens, ref_parents, bos, n_thr, args.cpu_streams,
+                                                      args.cpu_frames)
+        cpu_scores = float(Tc) * Sc * B * V / sec
+        log(f"oracle on {n_thr} threads: {sec:.1f}s, {cpu_scores:.3g} scores/s, agrees={agree}")
+        # the independent count of the algorithmic bytes, from the states the
+        # oracle's (replayed) decode visits
+        chk = None
+        if Sc == S and Tc == T:
+            visits = checker.visited_states(olm, otr, V, w.blank, B, r["tokens"], r["parents"])
+            chk, chk_steps = checker.algorithmic_bytes(w.lm, w.phrases, visits, T, beam=B > 1)
+            out["roofline"]["algorithmic_bytes_checker"] = chk
+            out["roofline"]["algorithmic_bytes_agree"] = bool(chk == alg_bytes and chk_steps == hyp_steps)
+            log(f"checker: {chk} algorithmic bytes over {chk_steps} hyp-steps (kernel {alg_bytes}, {hyp_steps})")
+        _, _, _, sec1, Sc1, Tc1, agree1, _ = cpu_leg(w, ref_tokens, ref_parents, bos, 1, args.cpu_streams_single,
+                                                     args.cpu_frames)
+        cpu1 = float(Tc1) * Sc1 * B * V / sec1
+        log(f"oracle on 1 thread: {sec1:.1f}s, {cpu1:.3g} scores/s")
         out["cpu_baseline"] = {
             "value": cpu_scores, "unit": "hyp×vocab scores/s", "cores": n_thr, "kind": "oracle",
             "sample": f"first {Tc} frames of {Sc} of the {S} streams (beam {B}), {Sc * B * Tc} hyp-steps, "
-                      f"{cpu_s:.1f}s; GPU decisions on the sample agree with the oracle: {agree} "
-                      f"(near ties accepted: {int(r['near_ties'].sum())})",
+                      f"{sec:.1f}s on {n_thr} threads (host threads capped at {HOST_THREADS_CAP}, the CPU share "
+                      f"of one GPU; {os.cpu_count()} logical CPUs visible); GPU decisions on the sample agree "
+                      f"with the oracle: {agree} (near ties accepted: {near})",
+            "cpu_model": cpu_model(),
+            "single_thread": {"value": cpu1, "unit": "hyp×vocab scores/s", "cores": 1,
+                              "sample": f"first {Tc1} frames of {Sc1} streams (beam {B}), {Sc1 * B * Tc1} hyp-steps, "
+                                        f"{sec1:.1f}s; agree: {agree1}"},
         }
-        log(f"oracle: {cpu_s:.1f}s, {cpu_scores:.3g} scores/s, agrees={agree}")
     print(json.dumps(out), flush=True)
 
 

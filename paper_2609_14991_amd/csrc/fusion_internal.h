@@ -31,7 +31,7 @@ namespace fusion {
 struct LMDevice {
   const float *dense = nullptr;        // [(V+2) * V]  level-1 row of every one-token context
   const int32_t *rec_dense = nullptr;  // [(V+2) * V * rec_stride]  record of the state after (w, y)
-  const int32_t *cnt1 = nullptr;       // [V+2]        explicit bigram successors with y < V
+  const int32_t *cnt1 = nullptr;       // [V+2]        explicit bigram successors (</s> included)
   const float *eos1 = nullptr;         // [V+2]        level-1 value of </s>: p*(w </s>), else uni(</s>) + bo(w)
   const int32_t *rec = nullptr;        // [(n_states - (V+2)) * rec_stride] state records
   const int2 *arcs = nullptr;          // (token, logp bits) of the arcs of levels 2..N-1, level by level

@@ -229,12 +229,12 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
       int64_t u = uni_row[w];
       if (u < 0) continue;
       int64_t beg = arc_beg[1][u], n = arc_cnt[1][u];
+      cnt1[w] = (int32_t)n;  // every explicit successor, </s> included (the fan-out of the traffic count)
       for (int64_t i = beg; i < beg + n; ++i) {
         int32_t y = tok_of(2, i, 1);
         if (y >= V) continue;
         row[y] = lp_of(2, i);
         nrow[y] = N >= 3 ? (int32_t)(d.off[2] + i) : y;
-        ++cnt1[w];
       }
     }
   });

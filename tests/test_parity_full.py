@@ -21,6 +21,7 @@ import torch
 
 import oracle
 import paper_2609_14991_amd as F
+from oracle import traffic as checker
 from workloads import load_workload
 
 pytestmark = pytest.mark.gpu
@@ -51,8 +52,9 @@ def beam_vs_oracle(w, label):
     bs = torch.zeros((H,), dtype=torch.int32, device=dev())
     sc0 = np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)
     sc = torch.from_numpy(sc0.copy()).to(dev())
+    kb = torch.zeros(2, dtype=torch.int64, device=dev())
     out = F.run(lm, trie, torch.from_numpy(w.logits).to(dev()), S, B, k, w.lam, w.beta, w.blank,
-                F.FUSION_BLANK_COMPETE, ls, bs, sc)
+                F.FUSION_BLANK_COMPETE, ls, bs, sc, traffic=kb)
     torch.cuda.synchronize()
     assert F.fusion_device_status() == 0
     tok = out["tokens"].cpu().numpy()
@@ -69,8 +71,20 @@ def beam_vs_oracle(w, label):
     assert np.array_equal(np.isfinite(got), fin), f"{label}: dead slots"
     err = np.abs(got[fin] - ref[fin]).max()
     assert err <= T * SCORE_TOL, f"{label}: final beam score error {err}"
+    check_traffic(w, olm, otr, r["tokens"], r["parents"], kb, label)
     print(f"{label}: {H} hypotheses x {T} frames agree; near ties {int(r['near_ties'].sum())}, "
           f"max final score error {err:.2e}")
+
+
+def check_traffic(w, olm, otr, tokens, parents, kb, label):
+    """The kernel's count of algorithmic bytes and hypothesis-steps equals the
+    independent count over the states the oracle's decode visits."""
+    visits = checker.visited_states(olm, otr, w.V, w.blank, w.B, tokens, parents)
+    alg, n = checker.algorithmic_bytes(w.lm, w.phrases, visits, w.T, beam=w.B > 1)
+    got = [int(v) for v in kb.cpu()]
+    assert got == [alg, n], f"{label}: kernel counts {got}, checker {[alg, n]}"
+    print(f"{label}: {alg} algorithmic bytes over {n} hypothesis-steps ({alg / n:.0f} B each), "
+          "kernel and checker agree")
 
 
 def test_c3_full_greedy():
@@ -81,8 +95,9 @@ def test_c3_full_greedy():
     H = w.H
     ls = torch.full((H,), bos, dtype=torch.int32, device=dev())
     bs = torch.zeros((H,), dtype=torch.int32, device=dev())
+    kb = torch.zeros(2, dtype=torch.int64, device=dev())
     out = F.run(lm, trie, torch.from_numpy(w.logits).to(dev()), w.S, 1, 1, w.lam, w.beta, w.blank,
-                F.FUSION_BLANK_AM, ls, bs)
+                F.FUSION_BLANK_AM, ls, bs, traffic=kb)
     torch.cuda.synchronize()
     assert F.fusion_device_status() == 0
     r = oracle.run(olm, otr, w.logits, w.S, 1, 1, w.lam, w.beta, w.blank, 0, [bos] * H, [0] * H,
@@ -92,6 +107,7 @@ def test_c3_full_greedy():
     assert np.array_equal(ls.cpu().numpy(), r["lm_state"])
     assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
     print(f"C3: {int((tok != w.blank).sum())} emissions over {tok.size} hypothesis-frames")
+    check_traffic(w, olm, otr, r["tokens"], None, kb, "C3")
 
 
 def test_c4_full_beam():
