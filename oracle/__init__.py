@@ -38,9 +38,10 @@ _lib = None
 def lib():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB):
+        path = os.environ.get("ORACLE_LIB", LIB)  # a sanitized build in the sanitizer test
+        if path == LIB and not os.path.exists(LIB):
             build_oracle()
-        L = ctypes.CDLL(LIB)
+        L = ctypes.CDLL(path)
         vp, i32p, i64p, f32p, f64p = (ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32),
                                       ctypes.POINTER(ctypes.c_int64),
                                       ctypes.POINTER(ctypes.c_float),

@@ -8,6 +8,7 @@
 #include <string>
 
 #include "fusion.h"
+#include "tables_host.h"
 
 namespace fusion {
 
@@ -42,17 +43,7 @@ struct LMDevice {
   int32_t N = 0, V = 0, blank = 0, rec_stride = 0, eos_ok = 0, pad = 0;
 };
 
-// record of a state of order m (int32 words):
-//   [0]                     c_1 | (m << 16)
-//   [1]                     state id
-//   [2 + 3*(L-2) + 0]       bo(c_L) as float bits      (L = 2..m)
-//   [2 + 3*(L-2) + 1]       first arc of c_L (index into arcs)
-//   [2 + 3*(L-2) + 2]       number of arcs of c_L
-// (a one-token state w has m = 1 and no level entries)
-inline int record_stride(int N) {
-  int w = 2 + 3 * (N > 2 ? N - 2 : 0);
-  return (w + 3) & ~3;  // 16-byte records
-}
+// (the record layout of a state: record_stride in tables_host.h)
 
 // ---------------------------------------------------------------------------
 // BoostTrie

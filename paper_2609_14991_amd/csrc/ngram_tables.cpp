@@ -1,61 +1,23 @@
 // ngram_load: raw per-order n-gram arrays -> device-resident NgramTables.
 //
 // The LM term of Eq. (1) is a backoff n-gram over sub-word tokens (Sec. III-C).
-// The builder sorts each order, checks the closure the backoff recursion
-// relies on, numbers the states canonically (see fusion.h) and lays the model
-// out for the fusion kernels:
-//   * dense level-1 rows (one V-wide row per one-token context, already
-//     resolved against the unigram row and the context's backoff),
-//   * sorted per-order arc arrays for contexts of two or more tokens,
-//   * one record per state that inlines its whole backoff chain.
+// build_lm_host (tables_host.cpp) validates the model, numbers its states and
+// lays it out; this file uploads the layout and owns the device memory.
 #include <algorithm>
-#include <cmath>
 #include <cstring>
-#include <thread>
 #include <vector>
 
 #include "fusion_internal.h"
+#include "tables_host.h"
 
 namespace {
-
-using u128 = unsigned __int128;
-
-int token_bits(int V) {
-  int b = 1;
-  while ((1 << b) < V + 2) ++b;
-  return b;
-}
-
-template <class F>
-void parallel_for(int64_t n, F &&f) {
-  unsigned hw = std::thread::hardware_concurrency();
-  int nt = (int)std::min<unsigned>(hw ? hw : 4, 16);
-  if (n < (int64_t)1 << 16) nt = 1;
-  if (nt <= 1) {
-    f((int64_t)0, n);
-    return;
-  }
-  std::vector<std::thread> th;
-  for (int i = 0; i < nt; ++i) {
-    int64_t a = n * i / nt, b = n * (i + 1) / nt;
-    th.emplace_back([&f, a, b] { f(a, b); });
-  }
-  for (auto &t : th) t.join();
-}
-
-struct Order {
-  int k = 0;
-  int64_t n = 0;
-  std::vector<u128> key;     // sorted packed rows
-  std::vector<int64_t> src;  // input row of each sorted key (empty: identity)
-  int64_t row(int64_t i) const { return src.empty() ? i : src[i]; }
-};
 
 struct DeviceUpload {
   NgramTables *t;
   hipStream_t stream;
-  template <class T>
-  int put(const std::vector<T> &h, const T **dst) {
+  template <class T, class D>
+  int put(const std::vector<T> &h, const D **dst) {
+    static_assert(sizeof(T) == sizeof(D), "host and device element sizes differ");
     void *p = nullptr;
     size_t bytes = std::max<size_t>(h.size() * sizeof(T), 16);
     hipError_t e = hipMalloc(&p, bytes);
@@ -66,7 +28,7 @@ struct DeviceUpload {
       e = hipMemcpyAsync(p, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice, stream);
       if (e != hipSuccess) return fusion::hip_error(e, "hipMemcpyAsync");
     }
-    *dst = (const T *)p;
+    *dst = (const D *)p;
     return FUSION_OK;
   }
 };
@@ -82,243 +44,31 @@ extern "C" void ngram_free(NgramTables *lm) {
 extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const int64_t *count,
                           const int32_t *const *tokens, const float *const *logp,
                           const float *const *backoff, hipStream_t stream, NgramTables **out) {
-  using fusion::set_error;
-  if (!out) return set_error(FUSION_E_ARG, "ngram_load: out is NULL");
+  if (!out) return fusion::set_error(FUSION_E_ARG, "ngram_load: out is NULL");
   *out = nullptr;
-  if (order < 2 || order > FUSION_MAX_ORDER)
-    return set_error(FUSION_E_UNSUPPORTED, "ngram_load: order must be in [2, " + std::to_string(FUSION_MAX_ORDER) + "]");
-  if (vocab < 2 || vocab > FUSION_MAX_VOCAB)
-    return set_error(FUSION_E_UNSUPPORTED, "ngram_load: vocab must be in [2, " + std::to_string(FUSION_MAX_VOCAB) + "]");
-  if (blank_id < 0 || blank_id >= vocab) return set_error(FUSION_E_ARG, "ngram_load: blank_id out of range");
-  if (!count || !tokens || !logp) return set_error(FUSION_E_ARG, "ngram_load: NULL table pointer");
-  const int N = order, V = vocab, BOS = V, EOS = V + 1;
-  const int b = token_bits(V);
-  std::vector<Order> ord(N + 1);
-  // ---- pack, validate, sort ------------------------------------------------
-  for (int k = 1; k <= N; ++k) {
-    Order &o = ord[k];
-    o.k = k;
-    o.n = count[k - 1];
-    if (o.n < 0 || o.n > INT32_MAX) return set_error(FUSION_E_ARG, "ngram_load: bad count for order " + std::to_string(k));
-    if (o.n > 0 && (!tokens[k - 1] || !logp[k - 1]))
-      return set_error(FUSION_E_ARG, "ngram_load: NULL array for order " + std::to_string(k));
-    o.key.resize(o.n);
-    const int32_t *tk = tokens[k - 1];
-    const float *lp = logp[k - 1];
-    const float *bo = (k < N && backoff) ? backoff[k - 1] : nullptr;
-    int bad = 0;
-    int64_t bad_row = -1;
-    for (int64_t i = 0; i < o.n; ++i) {
-      u128 key = 0;
-      for (int j = 0; j < k; ++j) {
-        int32_t t = tk[i * k + j];
-        if (t < 0 || t >= V + 2 || t == blank_id) {
-          bad = 1;
-          bad_row = i;
-        }
-        key = (key << b) | (u128)(uint32_t)(t & ((1 << b) - 1));
-      }
-      if (!std::isfinite(lp[i]) || (bo && !std::isfinite(bo[i]))) {
-        bad = 2;
-        bad_row = i;
-      }
-      o.key[i] = key;
-      if (bad) break;
-    }
-    if (bad == 1) return set_error(FUSION_E_LM_FORMAT, "ngram_load: order " + std::to_string(k) + " row " + std::to_string(bad_row) + ": token out of range or blank");
-    if (bad == 2) return set_error(FUSION_E_LM_FORMAT, "ngram_load: order " + std::to_string(k) + " row " + std::to_string(bad_row) + ": non-finite value");
-    bool sorted = true;
-    for (int64_t i = 1; i < o.n && sorted; ++i) sorted = o.key[i - 1] < o.key[i];
-    if (!sorted) {
-      std::vector<std::pair<u128, int64_t>> kv(o.n);
-      for (int64_t i = 0; i < o.n; ++i) kv[i] = {o.key[i], i};
-      std::sort(kv.begin(), kv.end());
-      o.src.resize(o.n);
-      for (int64_t i = 0; i < o.n; ++i) {
-        o.key[i] = kv[i].first;
-        o.src[i] = kv[i].second;
-        if (i > 0 && kv[i - 1].first == kv[i].first)
-          return set_error(FUSION_E_LM_FORMAT, "ngram_load: duplicate n-gram of order " + std::to_string(k));
-      }
-    }
-  }
-  auto tok_of = [&](int k, int64_t i, int j) -> int32_t {  // j-th token of sorted row i
-    return (int32_t)((ord[k].key[i] >> (b * (k - 1 - j))) & ((1u << b) - 1));
-  };
-  auto lp_of = [&](int k, int64_t i) { return logp[k - 1][ord[k].row(i)]; };
-  auto bo_of = [&](int k, int64_t i) -> float {
-    return (k < N && backoff && backoff[k - 1]) ? backoff[k - 1][ord[k].row(i)] : 0.0f;
-  };
-  // ---- unigrams ------------------------------------------------------------
-  std::vector<float> uni_lp(V + 2, 0.0f), uni_bo(V + 2, 0.0f);
-  std::vector<char> present(V + 2, 0);
-  for (int64_t i = 0; i < ord[1].n; ++i) {
-    int32_t w = tok_of(1, i, 0);
-    present[w] = 1;
-    uni_lp[w] = lp_of(1, i);
-    uni_bo[w] = bo_of(1, i);
-  }
-  for (int w = 0; w <= BOS; ++w)
-    if (w != blank_id && !present[w])
-      return set_error(FUSION_E_LM_FORMAT, "ngram_load: id " + std::to_string(w) + " has no unigram");
-  // ---- prefix closure and arc ranges: ctx k-1 -> [beg, beg+cnt) in order k --
-  std::vector<std::vector<int64_t>> arc_beg(N + 1), arc_cnt(N + 1);
-  for (int k = 2; k <= N; ++k) {
-    const Order &lo = ord[k - 1], &hi = ord[k];
-    arc_beg[k - 1].assign(lo.n, 0);
-    arc_cnt[k - 1].assign(lo.n, 0);
-    int64_t c = 0;
-    for (int64_t i = 0; i < hi.n; ++i) {
-      u128 pre = hi.key[i] >> b;
-      while (c < lo.n && lo.key[c] < pre) ++c;
-      if (c >= lo.n || lo.key[c] != pre)
-        return set_error(FUSION_E_LM_FORMAT, "ngram_load: an order-" + std::to_string(k) + " n-gram lacks its prefix");
-      if (arc_cnt[k - 1][c] == 0) arc_beg[k - 1][c] = i;
-      ++arc_cnt[k - 1][c];
-    }
-  }
-  // ---- suffix closure: order k row -> index of its (k-1)-token suffix --------
-  std::vector<std::vector<int64_t>> sfx(N + 1);
-  for (int k = 2; k <= N; ++k) {
-    const Order &lo = ord[k - 1], &hi = ord[k];
-    sfx[k].assign(hi.n, -1);
-    const u128 mask = (((u128)1) << (b * (k - 1))) - 1;
-    std::vector<int64_t> &s = sfx[k];
-    parallel_for(hi.n, [&](int64_t a, int64_t e) {
-      for (int64_t i = a; i < e; ++i) {
-        u128 suf = hi.key[i] & mask;
-        auto it = std::lower_bound(lo.key.begin(), lo.key.end(), suf);
-        if (it != lo.key.end() && *it == suf) s[i] = it - lo.key.begin();
-      }
-    });
-    for (int64_t i = 0; i < hi.n; ++i)
-      if (s[i] < 0) return set_error(FUSION_E_LM_FORMAT, "ngram_load: an order-" + std::to_string(k) + " n-gram lacks its suffix");
-  }
-  // ---- state numbering -------------------------------------------------------
+  fusion::LMHost h;
+  std::string why;
+  int rc = fusion::build_lm_host(order, vocab, blank_id, count, tokens, logp, backoff, &h, &why);
+  if (rc != FUSION_OK) return fusion::set_error(rc, why);
   auto *t = new NgramTables();
   fusion::LMDevice &d = t->dev;
-  d.N = N;
-  d.V = V;
-  d.blank = blank_id;
-  d.eos_ok = present[EOS];
-  d.off[2] = V + 2;
-  for (int k = 2; k <= N; ++k) d.off[k + 1] = d.off[k] + ord[k].n;
-  d.n_states = d.off[N];
-  if (d.n_states > INT32_MAX) {
-    delete t;
-    return set_error(FUSION_E_UNSUPPORTED, "ngram_load: more than 2^31 states");
-  }
-  for (int k = 1; k <= N; ++k) t->n[k] = ord[k].n;
-  d.rec_stride = fusion::record_stride(N);
-  const int RS = d.rec_stride;
-  // ---- dense level-1 rows ----------------------------------------------------
-  std::vector<float> dense((size_t)(V + 2) * V);
-  std::vector<int32_t> dense_next((size_t)(V + 2) * V);  // host only: state after (w, y)
-  std::vector<int32_t> cnt1(V + 2, 0);
-  std::vector<int64_t> uni_row(V + 2, -1);
-  for (int64_t i = 0; i < ord[1].n; ++i) uni_row[tok_of(1, i, 0)] = i;
-  parallel_for(V + 2, [&](int64_t a, int64_t e) {
-    for (int64_t w = a; w < e; ++w) {
-      float bw = uni_bo[w];
-      float *row = dense.data() + w * V;
-      int32_t *nrow = dense_next.data() + w * V;
-      for (int y = 0; y < V; ++y) {
-        row[y] = (y == blank_id) ? 0.0f : uni_lp[y] + bw;
-        nrow[y] = y;
-      }
-      int64_t u = uni_row[w];
-      if (u < 0) continue;
-      int64_t beg = arc_beg[1][u], n = arc_cnt[1][u];
-      cnt1[w] = (int32_t)n;  // every explicit successor, </s> included (the fan-out of the traffic count)
-      for (int64_t i = beg; i < beg + n; ++i) {
-        int32_t y = tok_of(2, i, 1);
-        if (y >= V) continue;
-        row[y] = lp_of(2, i);
-        nrow[y] = N >= 3 ? (int32_t)(d.off[2] + i) : y;
-      }
-    }
-  });
-  // ---- level-1 value of </s> per one-token context (the dense rows hold y < V) ----
-  std::vector<float> eos1(V + 2, 0.0f);
-  if (d.eos_ok) {
-    for (int64_t w = 0; w < V + 2; ++w) {
-      eos1[w] = uni_lp[EOS] + uni_bo[w];
-      const int64_t u = uni_row[w];
-      if (u < 0) continue;
-      const int64_t beg = arc_beg[1][u], n = arc_cnt[1][u];
-      if (n > 0 && tok_of(2, beg + n - 1, 1) == EOS) eos1[w] = lp_of(2, beg + n - 1);  // </s> sorts last
-    }
-  }
-  // ---- arcs of levels 2..N-1 (order L+1 n-grams), one array level by level -----
-  int64_t n_arcs = 0;
-  for (int L = 2; L <= N - 1; ++L) {
-    d.arc_base[L] = n_arcs;
-    n_arcs += ord[L + 1].n;
-  }
-  if (n_arcs > INT32_MAX) {
-    delete t;
-    return set_error(FUSION_E_UNSUPPORTED, "ngram_load: more than 2^31 n-grams of orders 3..N");
-  }
-  std::vector<int2> arcs((size_t)n_arcs);
-  for (int L = 2; L <= N - 1; ++L) {
-    const int k = L + 1;
-    int2 *A = arcs.data() + d.arc_base[L];
-    parallel_for(ord[k].n, [&](int64_t a, int64_t e) {
-      for (int64_t i = a; i < e; ++i) {
-        float p = lp_of(k, i);
-        int32_t bits;
-        std::memcpy(&bits, &p, 4);
-        A[i] = make_int2(tok_of(k, i, k - 1), bits);
-      }
-    });
-  }
-  // ---- state after an order-N arc --------------------------------------------
-  std::vector<int32_t> top_next(ord[N].n);
-  for (int64_t i = 0; i < ord[N].n; ++i)
-    top_next[i] = (N - 1 == 1) ? tok_of(N, i, N - 1) : (int32_t)(d.off[N - 1] + sfx[N][i]);
-  // ---- state records (orders 2..N-1) -----------------------------------------
-  std::vector<int32_t> rec((size_t)(d.n_states - (V + 2)) * RS, 0);
-  for (int m = 2; m <= N - 1; ++m) {
-    parallel_for(ord[m].n, [&](int64_t a, int64_t e) {
-      for (int64_t i = a; i < e; ++i) {
-        int32_t *r = rec.data() + (size_t)(d.off[m] - (V + 2) + i) * RS;
-        r[0] = tok_of(m, i, m - 1) | (m << 16);
-        r[1] = (int32_t)(d.off[m] + i);
-        if (m >= 3) {
-          const int32_t *sr = rec.data() + (size_t)(d.off[m - 1] - (V + 2) + sfx[m][i]) * RS;
-          std::memcpy(r + 2, sr + 2, sizeof(int32_t) * 3 * (m - 2));
-        }
-        float bo = bo_of(m, i);
-        std::memcpy(&r[2 + 3 * (m - 2)], &bo, 4);
-        r[2 + 3 * (m - 2) + 1] = (int32_t)(d.arc_base[m] + arc_beg[m][i]);
-        r[2 + 3 * (m - 2) + 2] = (int32_t)arc_cnt[m][i];
-      }
-    });
-  }
-  // ---- record of the state after (w, y) for every one-token context w ------
-  std::vector<int32_t> rec_dense((size_t)(V + 2) * V * RS, 0);
-  parallel_for((int64_t)(V + 2) * V, [&](int64_t a, int64_t e) {
-    for (int64_t i = a; i < e; ++i) {
-      const int32_t sid = dense_next[i];
-      int32_t *r = rec_dense.data() + (size_t)i * RS;
-      if (sid >= V + 2) {
-        std::memcpy(r, rec.data() + (size_t)(sid - (V + 2)) * RS, sizeof(int32_t) * RS);
-      } else {
-        r[0] = sid | (1 << 16);
-        r[1] = sid;
-      }
-    }
-  });
-  // ---- upload -------------------------------------------------------------------
+  d.N = h.N;
+  d.V = h.V;
+  d.blank = h.blank;
+  d.eos_ok = h.eos_ok;
+  d.rec_stride = h.rec_stride;
+  d.n_states = h.n_states;
+  std::memcpy(d.off, h.off, sizeof d.off);
+  std::memcpy(d.arc_base, h.arc_base, sizeof d.arc_base);
+  std::memcpy(t->n, h.n, sizeof t->n);
   DeviceUpload up{t, stream};
-  int rc = FUSION_OK;
-  if (rc == FUSION_OK) rc = up.put(dense, &d.dense);
-  if (rc == FUSION_OK) rc = up.put(rec_dense, &d.rec_dense);
-  if (rc == FUSION_OK) rc = up.put(cnt1, &d.cnt1);
-  if (rc == FUSION_OK) rc = up.put(eos1, &d.eos1);
-  if (rc == FUSION_OK) rc = up.put(rec, &d.rec);
-  if (rc == FUSION_OK) rc = up.put(arcs, &d.arcs);
-  if (rc == FUSION_OK) rc = up.put(top_next, &d.top_next);
+  if (rc == FUSION_OK) rc = up.put(h.dense, &d.dense);
+  if (rc == FUSION_OK) rc = up.put(h.rec_dense, &d.rec_dense);
+  if (rc == FUSION_OK) rc = up.put(h.cnt1, &d.cnt1);
+  if (rc == FUSION_OK) rc = up.put(h.eos1, &d.eos1);
+  if (rc == FUSION_OK) rc = up.put(h.rec, &d.rec);
+  if (rc == FUSION_OK) rc = up.put(h.arcs, &d.arcs);
+  if (rc == FUSION_OK) rc = up.put(h.top_next, &d.top_next);
   if (rc == FUSION_OK) {
     hipError_t e = hipStreamSynchronize(stream);
     if (e != hipSuccess) rc = fusion::hip_error(e, "hipStreamSynchronize");
