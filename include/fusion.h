@@ -77,7 +77,7 @@ enum { FUSION_STATUS_BAD_LM_STATE = 1, FUSION_STATUS_BAD_BOOST_STATE = 2,
        FUSION_STATUS_SYNC_TIMEOUT = 4 /* a beam stream's workgroups failed to meet (results invalid) */ };
 
 /* limits of this build */
-#define FUSION_MAX_ORDER 8   /* n-gram order N */
+#define FUSION_MAX_ORDER 6   /* n-gram order N (the per-level registers of the fusion kernel are sized for it) */
 #define FUSION_MAX_VOCAB 8190
 #define FUSION_MAX_K 8
 #define FUSION_MAX_BEAM 32
@@ -105,6 +105,11 @@ typedef struct BoostTrie BoostTrie;     /* opaque, device resident, immutable af
  * (k-1)-token prefix and suffix in the model.  Inputs are copied: the
  * caller may free them when the call returns (it synchronizes the stream).
  * On success *out owns its device memory until ngram_free().
+ * Contexts of two or more tokens with more than 1024 / (N - 2) successors get
+ * a pre-resolved LM row on the device (so that the remaining successors of
+ * any state fit one memory round trip); the environment variable
+ * FUSION_CONTEXT_ROW_MIN_ARCS, read at each call, replaces that threshold.
+ * Results do not depend on it.
  */
 int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const int64_t *count,
                const int32_t *const *tokens, const float *const *logp,

@@ -10,6 +10,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import sys
 import subprocess
 
 import numpy as np
@@ -142,8 +143,8 @@ class OracleLM:
             raise OracleError(_err())
         self._keep = None  # the oracle copied everything
 
-    def __del__(self):
-        if getattr(self, "h", None):
+    def __del__(self, _finalizing=sys.is_finalizing):
+        if getattr(self, "h", None) and not _finalizing():  # at interpreter exit the memory goes anyway
             lib().or_lm_free(self.h)
             self.h = None
 
@@ -194,8 +195,8 @@ class OracleTrie:
         if not self.h:
             raise OracleError(_err())
 
-    def __del__(self):
-        if getattr(self, "h", None):
+    def __del__(self, _finalizing=sys.is_finalizing):
+        if getattr(self, "h", None) and not _finalizing():  # at interpreter exit the memory goes anyway
             lib().or_trie_free(self.h)
             self.h = None
 

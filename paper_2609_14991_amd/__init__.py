@@ -151,8 +151,8 @@ class _Handle:
             getattr(lib(), self._free_fn)(self.h)
         self.h = None
 
-    def __del__(self):
-        if sys.is_finalizing():
+    def __del__(self, _finalizing=sys.is_finalizing):
+        if _finalizing():
             return
         try:
             self.close()

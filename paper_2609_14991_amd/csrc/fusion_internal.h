@@ -39,6 +39,10 @@ struct LMDevice {
   int64_t arc_base[FUSION_MAX_ORDER] = {};  // first arc of level L (arcs of order L+1 n-grams)
   const int32_t *top_next = nullptr;   // [n_N]  state after an order-N arc (index - arc_base[N-1])
   int64_t off[FUSION_MAX_ORDER + 2] = {};   // off[k] = first id of order-k states (k >= 2)
+  // context rows (contexts of two or more tokens with many successors):
+  const float *ctx_lm = nullptr;       // [n_ctx * V]  lm(y | context), resolved through all its levels
+  const int32_t *ctx_rec = nullptr;    // [n_ctx * V * rec_stride]  record of the state after (context, y)
+  int64_t n_ctx = 0;
   int64_t n_states = 0;
   int32_t N = 0, V = 0, blank = 0, rec_stride = 0, eos_ok = 0, pad = 0;
 };

@@ -53,7 +53,7 @@ int hip_error(hipError_t e, const char *what) {
 namespace {
 
 constexpr int kMaxWaves = 16;
-constexpr int kMaxLevels = FUSION_MAX_ORDER;  // context levels 1..N-1 <= 7
+constexpr int kMaxLevels = FUSION_MAX_ORDER;  // context levels 1..N-1 <= 5
 constexpr int kAux = 256;                     // LDS side tables: phrase transitions, top-level next states
 constexpr int kNodeLane = 32;                 // lanes 32..35 of the record word hold the phrase node
 constexpr int kLM1Lane = 40;                  // lanes 40..59 hold the second LM's record
@@ -134,6 +134,8 @@ typedef __attribute__((address_space(3))) void *lds_ptr_t;
 __device__ __forceinline__ int rec_bo_lane(int L) { return 2 + 3 * (L - 2); }
 __device__ __forceinline__ int rec_beg_lane(int L) { return 3 + 3 * (L - 2); }
 __device__ __forceinline__ int rec_cnt_lane(int L) { return 4 + 3 * (L - 2); }
+// the record word naming the chain's context row (record_ctx_word)
+__device__ __forceinline__ int rec_ctx_lane(int N) { return 2 + 3 * (N > 2 ? N - 2 : 0); }
 
 // ---- wave-level reductions with DPP moves (no LDS) ------------------------------
 // rows of 16 lanes: quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror,
@@ -154,6 +156,13 @@ __device__ __forceinline__ float row_sum(float v) {
   v = v + dpp_f<0x4E, 0xF>(0.0f, v);
   v = v + dpp_f<0x141, 0xF>(0.0f, v);
   return v + dpp_f<0x140, 0xF>(0.0f, v);
+}
+// uniform maximum over the wave (-0 and +0 may come out either way)
+__device__ __forceinline__ float wave_max_f(float v) {
+  v = row_max(v);
+  v = fmaxf(v, dpp_f<0x142, 0xA>(-INFINITY, v));
+  v = fmaxf(v, dpp_f<0x143, 0xC>(-INFINITY, v));
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 // uniform sum over the wave
 __device__ __forceinline__ float wave_sum(float v) {
@@ -220,9 +229,10 @@ __device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(
 // hypothesis state carried between frames (LDS, written by one lane)
 template <int NL>
 struct HypState {
-  // per LM: where the next state comes from (an id, or < 0: reached from c1p by
-  // token y), the parent's c_1, the last token of the context (-1: from the
-  // record), the id of the state scored this frame
+  // per LM: where the next state comes from (an id; -1: reached from c1p by
+  // token y; -(r + 2): reached from the context of context row r by token y),
+  // the parent's c_1, the last token of the context (-1: from the record), the
+  // id of the state scored this frame
   int lmsrc[NL], c1p[NL], c1[NL], cur_lm[NL];
   int qsrc, y, fl;  // phrase source, token; flags 1 alive, 2 invalid
   int cur_q;        // phrase state scored this frame
@@ -243,17 +253,28 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   constexpr int Vp = NC * 4 * W;
   constexpr int kUA = W >= 1024 ? 1 : 4;  // arcs per lane fetched in the second hop
   constexpr int kUD = W >= 1024 ? 1 : 2;  // phrase transitions per lane fetched in the second hop
+  constexpr bool CTX = NC == 1;  // context rows used (an 8192-wide row pair would not fit the LDS)
   extern __shared__ __align__(16) unsigned char dyn[];
   // LDS rows, one entry per token: per LM, the dense level-1 row and the winning
   // explicit arc (stamp << 48 | level << 45 | offset << 32 | value bits, kept by
   // an atomic max, so the highest level wins whatever the order of the writes);
   // the phrase transition overriding the root's (stamp << 16 | transition + 1).
   // The stamp is the frame's (t mod 2^15) + 1: entries of earlier frames compare
-  // lower and read as absent, so no per-frame clearing is needed
-  float *lmval = reinterpret_cast<float *>(dyn);                                             // [NL][Vp]
-  unsigned long long *arcw = reinterpret_cast<unsigned long long *>(dyn + 4 * NL * Vp);      // [NL][Vp]
-  uint32_t *ptag = reinterpret_cast<uint32_t *>(dyn + 12 * NL * Vp);
-  float *sE = reinterpret_cast<float *>(dyn + (12 * NL + 4) * Vp);  // sE[j + 1]: entry value of transition j
+  // lower and read as absent, so no per-frame clearing is needed.  Row NL of
+  // lmval holds the first LM's context row when its state has one: the LM row of
+  // the deepest context of the chain with many successors, already resolved
+  // through every level up to that context
+  // With one LM the phrase term reads erow: per token the entry value E of the
+  // phrase state after it, the root's unless this frame's phrase state
+  // overrides the token.  Each lane puts its tokens back to the root's values
+  // right after reading them, and the scatter writes the overrides.
+  constexpr bool ER = NL == 1 && NC == 1;  // (8192-wide rows: no room in the LDS)
+  constexpr int kRows = NL + (CTX ? 1 : 0);
+  float *lmval = reinterpret_cast<float *>(dyn);                                                  // [kRows][Vp]
+  unsigned long long *arcw = reinterpret_cast<unsigned long long *>(dyn + 4 * kRows * Vp);        // [NL][Vp]
+  uint32_t *ptag = reinterpret_cast<uint32_t *>(dyn + (4 * kRows + 8 * NL) * Vp);
+  float *erow = reinterpret_cast<float *>(dyn + (4 * kRows + 8 * NL + 4) * Vp);                   // [Vp] if ER
+  float *sE = reinterpret_cast<float *>(dyn + (4 * kRows + 8 * NL + 4 + (ER ? 4 : 0)) * Vp);  // sE[j + 1]: entry value of transition j
   int *sDT = reinterpret_cast<int *>(sE + kAux + 4);
   int *sTN = sDT + kAux;  // [NL][kAux]
   __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves];
@@ -377,6 +398,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const int y0 = (c * W + g) * 4;
 #pragma unroll
     for (int j = 0; j < 4; ++j) rE[c][j] = (p.has_trie && y0 + j < p.V) ? tr.root_E[y0 + j] : 0.0f;
+    if (ER) *reinterpret_cast<float4 *>(erow + y0) = make_float4(rE[c][0], rE[c][1], rE[c][2], rE[c][3]);
   }
   clear_rows();
   __syncthreads();
@@ -398,31 +420,32 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
     }
   };
-  auto fetch_logits = [&](int tt) {
-    const rsrc_t xr = row_rsrc(p.logits + ((int64_t)tt * H + h) * p.V, p.V);
+  // the logits row of this hypothesis at the frame being fetched; it advances by
+  // one frame (H rows) per fetch and stays on the last frame
+  const float *xrow = p.logits + (int64_t)h * p.V;
+  const int64_t xstride = (int64_t)H * p.V;
+  auto fetch_logits = [&]() {
+    const rsrc_t xr = row_rsrc(xrow, p.V);
     fetch_strip(xr, xraw, voff);
     if (NW > 1 && wave == 1) fetch_strip(xr, xraw0, lane * 16);
   };
-  fetch_logits(0);
+  fetch_logits();
   // row statistics of the logits of strip sw (the 64-lane strip of wave sw) held
   // in xs: strip max, sum of exp below it, lowest id holding the max (only the
   // acoustic blank decision needs it).  They depend on the logits alone, so those
   // of frame t+1 are computed in frame t by the waves that are otherwise idle
   // while wave 0 ends the frame (wave 1 takes wave 0's strip); frame 0's here
   auto row_stats = [&](const float (&xs)[NC][4], int sw, int V) {
-    float xv[NC][4];
-    int xo[NC][4];  // order-preserving images of the logits (tokens >= V: -inf)
-    int lmx = INT_MIN;
+    float xv[NC][4];  // tokens >= V: -inf
+    float lmx = -INFINITY;
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         xv[c][j] = (c * W + sw * 64 + lane) * 4 + j < V ? xs[c][j] : -INFINITY;
-        xo[c][j] = ord_key(xv[c][j]);
-        lmx = max(lmx, xo[c][j]);
+        lmx = fmaxf(lmx, xv[c][j]);
       }
-    const int mwo = wave_max_i(lmx);
-    const float mw = key_of(mwo);
+    const float mw = wave_max_f(lmx);
     float lsum = 0.0f;
     if (mw > -INFINITY) {
 #pragma unroll
@@ -437,7 +460,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       for (int c = NC - 1; c >= 0; --c) {
         unsigned long long mj[4];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) mj[j] = __ballot(xo[c][j] == mwo && (c * W + sw * 64 + lane) * 4 + j < V);
+        for (int j = 0; j < 4; ++j) mj[j] = __ballot(xv[c][j] == mw && (c * W + sw * 64 + lane) * 4 + j < V);
         const unsigned long long any = mj[0] | mj[1] | mj[2] | mj[3];
         if (any) {
           const int src = __ffsll((long long)any) - 1;
@@ -454,11 +477,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       s_paid[sw] = aid;
     }
   };
-  // the level-1 dense row of LM i for context token cc straight into its LDS row
-  // (this wave's strips)
-  auto load_dense = [&](int i, int cc, int V) {
-    const float *drow = lms[i].dense + (int64_t)cc * V;
-    float *row = lmval + i * Vp;
+  // a V-wide fp32 row straight from HBM into an LDS row (this wave's strips)
+  auto load_row = [&](const float *drow, float *row, int V) {
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int wbase = c * W + wave * 64;  // first 4-token strip of this wave
@@ -503,7 +523,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     for (int i = 0; i < NL; ++i) {
       rp[i] = nullptr;
       if (ok) {
-        if (lmsrc[i] < 0) rp[i] = lms[i].rec_dense + ((int64_t)uni(hs.c1p[i]) * V + yin) * RSl[i];
+        if (lmsrc[i] < -1) rp[i] = lms[i].ctx_rec + ((int64_t)(-lmsrc[i] - 2) * V + yin) * RSl[i];
+        else if (lmsrc[i] < 0) rp[i] = lms[i].rec_dense + ((int64_t)uni(hs.c1p[i]) * V + yin) * RSl[i];
         else if (lmsrc[i] >= V + 2) rp[i] = lms[i].rec + (int64_t)(lmsrc[i] - V - 2) * RSl[i];
       }
     }
@@ -541,7 +562,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       // unconditionally (row 0 stands in when the hypothesis has no keys to
       // compute this frame), so that the record decode can wait for the record
       // alone
-      load_dense(i, ok ? c1[i] : 0, V);
+      load_row(lms[i].dense + (int64_t)(ok ? c1[i] : 0) * V, lmval + i * Vp, V);
     }
     if (NW == 1 && t > 0) row_stats(xraw, 0, V);  // a single wave has no idle helper
     // ---- decode the records ---------------------------------------------------------
@@ -555,7 +576,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     // levels 2..7 as uniform values (readlane at fixed lanes is valid whatever
     // the active mask); adding the zero backoffs above m changes no sum (at most
     // the sign of a zero)
-    int m[NL], sid[NL], total_arcs[NL];
+    // The first LM's context row (level D >= 2 of the chain, row r) replaces the
+    // levels up to D: only the arcs of the levels above D are fetched (lcnt 0
+    // for the others).  Further LMs fetch the arcs of every level.
+    int m[NL], sid[NL], total_arcs[NL], Dc = 0, crow = 0;
     float bo[NL][kMaxLevels];
     int lcnt[NL][kMaxLevels], lbeg[NL][kMaxLevels];
 #pragma unroll
@@ -563,15 +587,25 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       const int l0 = rec_lane0(i);
       m[i] = rp[i] ? (rdl(rw, l0) >> 16) : 1;
       sid[i] = rp[i] ? rdl(rw, l0 + 1) : lmsrc[i];
+      int Di = 0;
+      if (CTX && i == 0 && rp[0]) {
+        const int cw = rdl(rw, rec_ctx_lane(Nl[0]));
+        Dc = Di = (int)((unsigned)cw >> 28);
+        crow = cw & 0x0FFFFFFF;
+      }
       total_arcs[i] = 0;
+      // levels above m are absent: backoff 0 and no arcs (their record words
+      // hold zeros or, at level N, the context-row word)
 #pragma unroll
       for (int L = 2; L < kMaxLevels; ++L) {
-        bo[i][L] = as_float(rdl(rw, l0 + rec_bo_lane(L)));
-        lcnt[i][L] = rdl(rw, l0 + rec_cnt_lane(L));
-        lbeg[i][L] = rdl(rw, l0 + rec_beg_lane(L));
+        const bool lv = L <= m[i];
+        bo[i][L] = lv ? as_float(rdl(rw, l0 + rec_bo_lane(L))) : 0.0f;
+        lcnt[i][L] = (lv && L > Di) ? rdl(rw, l0 + rec_cnt_lane(L)) : 0;
+        lbeg[i][L] = lv ? rdl(rw, l0 + rec_beg_lane(L)) : 0;
         total_arcs[i] += lcnt[i][L];
       }
     }
+    if (CTX && ok && Dc >= 2) load_row(lms[0].ctx_lm + (int64_t)crow * V, lmval + NL * Vp, V);
     // ---- hop 2: first arcs of levels 2..m (flattened) and first phrase transitions --
     int2 ab[NL][kUA];
     int at[NL][kUA], tn[NL][kUA];  // at = level << 16 | offset within the level
@@ -587,6 +621,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         int L = 2, bL = lbeg[i][2];
 #pragma unroll
         for (int L2 = 2; L2 < kMaxLevels - 1; ++L2) {
+          if (L2 >= m[i]) break;  // uniform: no arcs above m
           const bool past = (L == L2) && (f >= lcnt[i][L2]);
           f = past ? f - lcnt[i][L2] : f;
           L = past ? L2 + 1 : L;
@@ -624,7 +659,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       if (y < V) {
         float v = as_float(a.y);
 #pragma unroll
-        for (int L2 = 3; L2 < kMaxLevels; ++L2) v = v + (L2 > L ? bo[i][L2] : 0.0f);
+        for (int L2 = 3; L2 < kMaxLevels; ++L2) {
+          if (L2 > m[i]) break;  // uniform: the levels above m back off by nothing
+          v = v + (L2 > L ? bo[i][L2] : 0.0f);
+        }
         const uint32_t tag = (stamp << 16) | (uint32_t)((L << 13) | j);
         __hip_atomic_fetch_max(arcw + i * Vp + y, ((unsigned long long)tag << 32) | (unsigned long long)__float_as_uint(v),
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -637,6 +675,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const int j = u * W + g;
         if (j < dcnt) {
           ptag[dd[u].x] = (stamp << 16) | (uint32_t)(j + 1);
+          if (ER) erow[dd[u].x] = as_float(dd[u].z);
           if (j < kAux) {
             sE[j + 1] = as_float(dd[u].z);
             sDT[j] = dd[u].y;
@@ -646,6 +685,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       for (int j = kUD * W + g; j < dcnt; j += W) {
         const int4 e = tr.delta[dbeg + j];
         ptag[e.x] = (stamp << 16) | (uint32_t)(j + 1);
+        if (ER) erow[e.x] = as_float(e.z);
         if (j < kAux) {
           sE[j + 1] = as_float(e.z);
           sDT[j] = e.y;
@@ -662,7 +702,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const int l0 = rec_lane0(i), N = Nl[i];
         int covered = kUA * W;
         for (int L = 2; L <= m[i]; ++L) {
-          const int bL = rdl(rw, l0 + rec_beg_lane(L)), cL = rdl(rw, l0 + rec_cnt_lane(L));
+          const int bL = rdl(rw, l0 + rec_beg_lane(L));
+          const int cL = (i != 0 || L > Dc) ? rdl(rw, l0 + rec_cnt_lane(L)) : 0;
           const int done = min(cL, max(0, covered));
           covered -= cL;
           const int2 *A = lms[i].arcs + bL;
@@ -687,15 +728,16 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     __builtin_amdgcn_s_waitcnt(0);  // the dense rows have landed in LDS
     __syncthreads();
     // ---- combine the row statistics (lanes 0..NW-1 hold one wave each) --------------
-    float lse;
-    int am;
-    {
+    // the log-sum-exp is needed by wave 0 (selected scores, beam totals) and, for
+    // fused rows, by every wave; the acoustic argmax (mode A) by every wave
+    float lse = 0.0f;
+    int am = INT_MAX;
+    if (wave == 0 || p.fused != nullptr || p.mode == FUSION_BLANK_AM) {
       const bool wl = lane < NW;
       const float pm = wl ? s_pm[lane] : -INFINITY;
       const float M = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_max(pm)), 0));
       const float term = (wl && pm > -INFINITY) ? s_ps[lane] * exp_fast(pm - M) : 0.0f;
       lse = M + logf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_sum(term)), 0)));
-      am = INT_MAX;
       if (p.mode == FUSION_BLANK_AM) {
         float ak = pm;
         int ay = wl ? s_paid[lane] : INT_MAX;
@@ -727,45 +769,51 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         kk[c][j] = xv[c][j];
       }
       if (want_keys) {
-        const uint4 p4 = *reinterpret_cast<const uint4 *>(ptag + y0);
         uint32_t aw[NL][4], av[NL][4];  // tag and value halves of the arc entries
         float lv[NL][4];                // dense rows
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
           const uint4 a01 = *reinterpret_cast<const uint4 *>(arcw + i * Vp + y0);
           const uint4 a23 = *reinterpret_cast<const uint4 *>(arcw + i * Vp + y0 + 2);
-          const float4 l4 = *reinterpret_cast<const float4 *>(lmval + i * Vp + y0);
+          const float4 l4 = *reinterpret_cast<const float4 *>(lmval + (CTX && i == 0 && Dc >= 2 ? NL : i) * Vp + y0);
           aw[i][0] = a01.y; aw[i][1] = a01.w; aw[i][2] = a23.y; aw[i][3] = a23.w;
           av[i][0] = a01.x; av[i][1] = a01.z; av[i][2] = a23.x; av[i][3] = a23.z;
           lv[i][0] = l4.x; lv[i][1] = l4.y; lv[i][2] = l4.z; lv[i][3] = l4.w;
         }
-        // transition + 1 of this frame's phrase entry, 0 if none
-        uint32_t hi[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t pw = j == 0 ? p4.x : j == 1 ? p4.y : j == 2 ? p4.z : p4.w;
-          hi[j] = (pw >> 16) == stamp ? (pw & 0xFFFFu) : 0u;
-        }
-        // the phrase entry values: the LDS copy of the state's first kAux transitions
-        // (read for every token, index 0 when unused, so that no per-token branch
-        // guards the read), the delta table beyond them only for a state with more
         float eh[4];
+        uint32_t hi[4];
+        if constexpr (ER) {
+          const float4 ev4 = *reinterpret_cast<const float4 *>(erow + y0);
+          eh[0] = ev4.x; eh[1] = ev4.y; eh[2] = ev4.z; eh[3] = ev4.w;
+        } else {
+          // transition + 1 of this frame's phrase entry, 0 if none
+          const uint4 p4 = *reinterpret_cast<const uint4 *>(ptag + y0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) eh[j] = sE[min((int)hi[j], kAux)];
-        asm volatile("" ::"v"(eh[0]), "v"(eh[1]), "v"(eh[2]), "v"(eh[3]));
-        if (dcnt > kAux) {
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t pw = j == 0 ? p4.x : j == 1 ? p4.y : j == 2 ? p4.z : p4.w;
+            hi[j] = (pw >> 16) == stamp ? (pw & 0xFFFFu) : 0u;
+          }
+          // the phrase entry values: the LDS copy of the state's first kAux transitions
+          // (read for every token, index 0 when unused, so that no per-token branch
+          // guards the read), the delta table beyond them only for a state with more
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (hi[j] > (uint32_t)kAux) eh[j] = as_float(tr.delta[dbeg + (int)hi[j] - 1].z);
+          for (int j = 0; j < 4; ++j) eh[j] = sE[min((int)hi[j], kAux)];
+          asm volatile("" ::"v"(eh[0]), "v"(eh[1]), "v"(eh[2]), "v"(eh[3]));
+          if (dcnt > kAux) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              if (hi[j] > (uint32_t)kAux) eh[j] = as_float(tr.delta[dbeg + (int)hi[j] - 1].z);
+          }
         }
-        // per LM, the dense row plus the backoffs of levels 2..m in increasing
-        // order (the levels above m back off by 0)
+        // per LM, the dense row (the first LM's context row when it has one) plus
+        // the backoffs of the levels above it up to m, in increasing order (the
+        // levels above m back off by 0)
         float dres[NL][4];
 #pragma unroll
         for (int i = 0; i < NL; ++i) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) dres[i][j] = lv[i][j];
-          for (int L2 = 2; L2 <= m[i]; ++L2) {
+          for (int L2 = (CTX && i == 0 && Dc >= 2) ? Dc + 1 : 2; L2 <= m[i]; ++L2) {
             const float b2 = as_float(rdl(rw, rec_lane0(i) + rec_bo_lane(L2)));
 #pragma unroll
             for (int j = 0; j < 4; ++j) dres[i][j] = dres[i][j] + b2;
@@ -785,13 +833,16 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
             const float a1 = p.lam[i] * lmv;
             u = u + a1;
           }
-          // phrases: the transition's entry value if this state overrides y, else the root's
-          const float e = hi[j] ? eh[j] : rE[c][j];
+          // phrases: the transition's entry value if this state overrides y, else the
+          // root's (with no phrase tree both are 0 and so is phi)
+          const float e = ER ? eh[j] : (hi[j] ? eh[j] : rE[c][j]);
           const float bst = e - phiq;
-          const float a3 = p.beta * (p.has_trie ? bst : 0.0f);
+          const float a3 = p.beta * ((ER || p.has_trie) ? bst : 0.0f);
           kk[c][j] = (y == blank) ? x : u + a3;
         }
       }
+      // this lane's entry values back to the root's for the next frame (read above)
+      if (ER) *reinterpret_cast<float4 *>(erow + y0) = make_float4(rE[c][0], rE[c][1], rE[c][2], rE[c][3]);
       if (write_fused && y0 < V) {
         if (AL) {
           row_store4(fr, make_float4(kk[c][0] - lse, kk[c][1] - lse, kk[c][2] - lse, kk[c][3] - lse), voff, c * W * 16);
@@ -806,7 +857,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     // than beside the frame-start loads, whose burst sets the start of the frame.
     // Unconditional (the last frame fetches its own row again): a conditional
     // fetch would make the compiler wait for it where the branches join
-    fetch_logits(min(t + 1, p.T - 1));
+    if (t + 1 < p.T) xrow += xstride;
+    fetch_logits();
     // ---- the wave's top-k: per round the wave maximum of the remaining keys, then
     // the lowest id holding it (ties to the lowest id).  Keys compete as
     // order-preserving ints; tokens that are not candidates or are already taken
@@ -1047,7 +1099,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         for (int i = 0; i < NL; ++i) {
           const uint32_t aw = (uint32_t)(arcw[i * Vp + cy] >> 32);
           const uint32_t lo = (aw >> 16) == stamp ? (aw & 0xFFFFu) : 0u;
-          cl[i] = -1;
+          // -1: the state after (c_1, y) (rec_dense); -(r + 2): the state after
+          // (context of row r, y) (ctx_rec)
+          cl[i] = (CTX && i == 0 && Dc >= 2) ? -(crow + 2) : -1;
           if (lo) {
             const int L = (int)(lo >> 13), jj = (int)(lo & 0x1FFFu), N = Nl[i];
             const int bL = s_lbeg[i][L];
@@ -1082,7 +1136,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 #pragma unroll
             for (int i = 0; i < NL; ++i) {
               int l = cl[i];
-              if (!inv && l < 0) l = lms[i].rec_dense[((int64_t)hs.c1[i] * V + cy) * RSl[i] + 1];
+              if (!inv && l < -1) l = lms[i].ctx_rec[((int64_t)(-l - 2) * V + cy) * RSl[i] + 1];
+              else if (!inv && l < 0) l = lms[i].rec_dense[((int64_t)hs.c1[i] * V + cy) * RSl[i] + 1];
               p.next_lm[(int64_t)i * H * K + o] = l;
             }
             if (!inv && q < 0) q = tr.root_node[cy].w;
@@ -1320,7 +1375,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
       int nl = hs.lmsrc[i];
-      if (moved && nl < 0) nl = lms[i].rec_dense[((int64_t)hs.c1p[i] * V + y) * RSl[i] + 1];
+      if (moved && nl < -1) nl = lms[i].ctx_rec[((int64_t)(-nl - 2) * V + y) * RSl[i] + 1];
+      else if (moved && nl < 0) nl = lms[i].rec_dense[((int64_t)hs.c1p[i] * V + y) * RSl[i] + 1];
       p.lm_state[(int64_t)i * H + h] = nl;
     }
     if (moved && nq < 0) nq = tr.root_node[y].w;
@@ -1390,10 +1446,13 @@ KernelFn pick(const Shape &sh, int km, bool al, int mode, int n_lm) {
   return pick_k<1024, 2, 1>(km, al, mode);
 }
 
-// dynamic LDS of a launch: per LM the dense row and the arc entries, the phrase
-// entries, the phrase side tables and per LM the top-level next states
+// dynamic LDS of a launch: per LM the dense row and the arc entries, the first
+// LM's context row (rows of at most 4096 tokens), the phrase entries, with one LM
+// the phrase entry values (rows of at most 4096 tokens), the phrase side tables
+// and per LM the top-level next states
 size_t dyn_lds_bytes(int Vp, int n_lm) {
-  return (size_t)Vp * (12 * n_lm + 4) + (size_t)4 * (kAux * (2 + n_lm) + 4);
+  return (size_t)Vp * (12 * n_lm + 4 + (Vp <= 4096 ? 4 : 0) + (n_lm == 1 && Vp <= 4096 ? 4 : 0)) +
+         (size_t)4 * (kAux * (2 + n_lm) + 4);
 }
 
 struct DeviceInfo {
@@ -1449,14 +1508,15 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   if (e != hipSuccess) return hip_error(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
   const long resident = (long)per_cu * di.cus;
   int s_batch = (int)std::min<long>(p.S, resident / p.B);
+  // exchange records: 2 buffers x B x k candidates x (3 + n_lm (+1 recombining)) words per stream
+  const size_t stream_words = (size_t)2 * p.B * p.k * (3 + p.n_lm + (p.recombine ? 1 : 0));
   if (s_batch >= 8) s_batch -= s_batch % 8;
   if (s_batch < 1) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device at once");
-  // exchange records: 2 buffers x B x k candidates x (3 + n_lm (+1 recombining)) words per stream
-  const size_t xwords = (size_t)s_batch * 2 * p.B * p.k * (3 + p.n_lm + (p.recombine ? 1 : 0));
-  void *scratch = nullptr;
-  e = hipMallocAsync(&scratch, xwords * sizeof(unsigned long long), stream);
+  const size_t xwords = (size_t)s_batch * stream_words;
+  void *xbuf = nullptr;
+  e = hipMallocAsync(&xbuf, xwords * sizeof(unsigned long long), stream);
   if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
-  p.xchg = reinterpret_cast<unsigned long long *>(scratch);
+  p.xchg = reinterpret_cast<unsigned long long *>(xbuf);
   int rc = FUSION_OK;
   for (int s0 = 0; s0 < p.S && rc == FUSION_OK; s0 += s_batch) {
     const int ns = std::min(s_batch, p.S - s0);
@@ -1464,7 +1524,7 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
     // nor an earlier batch's records can pass for the current frame's
     const int n_ints = (int)(xwords * 2);
     hipLaunchKernelGGL(zero_ints, dim3(std::min(64, (n_ints + 255) / 256)), dim3(256), 0, stream,
-                       reinterpret_cast<int *>(scratch), n_ints);
+                       reinterpret_cast<int *>(xbuf), n_ints);
     e = hipGetLastError();
     if (e != hipSuccess) {
       rc = hip_error(e, "exchange reset launch");
@@ -1477,7 +1537,7 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(ns * p.B), dim3(sh.W), args, dyn, stream);
     if (e != hipSuccess) rc = hip_error(e, "cooperative fusion kernel launch");
   }
-  hipError_t e2 = hipFreeAsync(scratch, stream);
+  hipError_t e2 = hipFreeAsync(xbuf, stream);
   if (rc == FUSION_OK && e2 != hipSuccess) rc = hip_error(e2, "hipFreeAsync");
   return rc;
 }

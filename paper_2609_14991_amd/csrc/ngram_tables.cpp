@@ -58,6 +58,7 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
   d.eos_ok = h.eos_ok;
   d.rec_stride = h.rec_stride;
   d.n_states = h.n_states;
+  d.n_ctx = h.n_ctx;
   std::memcpy(d.off, h.off, sizeof d.off);
   std::memcpy(d.arc_base, h.arc_base, sizeof d.arc_base);
   std::memcpy(t->n, h.n, sizeof t->n);
@@ -69,6 +70,8 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
   if (rc == FUSION_OK) rc = up.put(h.rec, &d.rec);
   if (rc == FUSION_OK) rc = up.put(h.arcs, &d.arcs);
   if (rc == FUSION_OK) rc = up.put(h.top_next, &d.top_next);
+  if (rc == FUSION_OK) rc = up.put(h.ctx_lm, &d.ctx_lm);
+  if (rc == FUSION_OK) rc = up.put(h.ctx_rec, &d.ctx_rec);
   if (rc == FUSION_OK) {
     hipError_t e = hipStreamSynchronize(stream);
     if (e != hipSuccess) rc = fusion::hip_error(e, "hipStreamSynchronize");

@@ -25,6 +25,7 @@
 #include <algorithm>
 #include <climits>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <thread>
@@ -66,6 +67,16 @@ struct Order {
 };
 
 }  // namespace
+
+int64_t context_row_min_arcs(int N) {
+  const char *env = std::getenv("FUSION_CONTEXT_ROW_MIN_ARCS");
+  if (env && *env) {
+    char *end = nullptr;
+    const long long v = std::strtoll(env, &end, 10);
+    if (end && *end == 0 && v >= 0) return (int64_t)v;
+  }
+  return N > 2 ? 1024 / (N - 2) : INT32_MAX;
+}
 
 int build_lm_host(int32_t order, int32_t vocab, int32_t blank_id, const int64_t *count,
                   const int32_t *const *tokens, const float *const *logp, const float *const *backoff,
@@ -263,6 +274,21 @@ int build_lm_host(int32_t order, int32_t vocab, int32_t blank_id, const int64_t 
   top_next.assign(ord[N].n, 0);
   for (int64_t i = 0; i < ord[N].n; ++i)
     top_next[i] = (N - 1 == 1) ? tok_of(N, i, N - 1) : (int32_t)(d.off[N - 1] + sfx[N][i]);
+  // ---- contexts that get a context row (more than X successors) -----------
+  const int64_t X = context_row_min_arcs(N);
+  const int CW = record_ctx_word(N);
+  std::vector<std::vector<int32_t>> ctx_of(N);  // [L][i]: row of the order-L context i, or -1
+  std::vector<std::pair<int, int64_t>> ctx_list;   // row -> (L, i)
+  for (int L = 2; L <= N - 1; ++L) {
+    ctx_of[L].assign(ord[L].n, -1);
+    for (int64_t i = 0; i < ord[L].n; ++i)
+      if (arc_cnt[L][i] > X) {
+        ctx_of[L][i] = (int32_t)ctx_list.size();
+        ctx_list.push_back({L, i});
+      }
+  }
+  if ((int64_t)ctx_list.size() >= ((int64_t)1 << 28)) return reject(FUSION_E_UNSUPPORTED, "ngram_load: too many context rows");
+  d.n_ctx = (int64_t)ctx_list.size();
   // ---- state records (orders 2..N-1) -----------------------------------------
   std::vector<int32_t> &rec = d.rec;
   rec.assign((size_t)(d.n_states - (V + 2)) * RS, 0);
@@ -280,9 +306,55 @@ int build_lm_host(int32_t order, int32_t vocab, int32_t blank_id, const int64_t 
         std::memcpy(&r[2 + 3 * (m - 2)], &bo, 4);
         r[2 + 3 * (m - 2) + 1] = (int32_t)(d.arc_base[m] + arc_beg[m][i]);
         r[2 + 3 * (m - 2) + 2] = (int32_t)arc_cnt[m][i];
+        // the deepest context row of the chain: this state's own, else its suffix's
+        const int32_t cr = ctx_of[m][i];
+        if (cr >= 0) r[CW] = (m << 28) | cr;
+        else if (m >= 3) r[CW] = rec[(size_t)(d.off[m - 1] - (V + 2) + sfx[m][i]) * RS + CW];
       }
     });
   }
+  // ---- context rows: the LM row of each such context and the state after each token --
+  // Level by level from the context's last token: row_1 = the dense level-1
+  // row; row_j(y) = p*(c_j y) for an arc of c_j, else row_{j-1}(y) + bo(c_j),
+  // one fp32 addition (the backoff recursion's order).  The state after y is
+  // the arc's state at the longest level with an arc, else the level-1 one.
+  d.ctx_lm.assign((size_t)d.n_ctx * V, 0.0f);
+  d.ctx_rec.assign((size_t)d.n_ctx * V * RS, 0);
+  parallel_for(d.n_ctx, [&](int64_t a, int64_t e) {
+    std::vector<float> row(V);
+    std::vector<int32_t> nxt(V);
+    int64_t idx[FUSION_MAX_ORDER + 1];
+    for (int64_t c = a; c < e; ++c) {
+      const int L = ctx_list[c].first;
+      idx[L] = ctx_list[c].second;
+      for (int j = L; j >= 3; --j) idx[j - 1] = sfx[j][idx[j]];
+      const int32_t w = tok_of(L, idx[L], L - 1);
+      std::memcpy(row.data(), dense.data() + (size_t)w * V, sizeof(float) * V);
+      std::memcpy(nxt.data(), dense_next.data() + (size_t)w * V, sizeof(int32_t) * V);
+      for (int j = 2; j <= L; ++j) {
+        const float bj = bo_of(j, idx[j]);
+        for (int y = 0; y < V; ++y) row[y] = row[y] + bj;
+        const int64_t beg = arc_beg[j][idx[j]], n = arc_cnt[j][idx[j]];
+        for (int64_t u = beg; u < beg + n; ++u) {
+          const int32_t y = tok_of(j + 1, u, j);
+          if (y >= V) continue;
+          row[y] = lp_of(j + 1, u);
+          nxt[y] = (j + 1 <= N - 1) ? (int32_t)(d.off[j + 1] + u) : top_next[u];
+        }
+      }
+      std::memcpy(d.ctx_lm.data() + (size_t)c * V, row.data(), sizeof(float) * V);
+      for (int y = 0; y < V; ++y) {
+        int32_t *r = d.ctx_rec.data() + ((size_t)c * V + y) * RS;
+        const int32_t sid = nxt[y];
+        if (sid >= V + 2) {
+          std::memcpy(r, rec.data() + (size_t)(sid - (V + 2)) * RS, sizeof(int32_t) * RS);
+        } else {
+          r[0] = sid | (1 << 16);
+          r[1] = sid;
+        }
+      }
+    }
+  });
   // ---- record of the state after (w, y) for every one-token context w ------
   std::vector<int32_t> &rec_dense = d.rec_dense;
   rec_dense.assign((size_t)(V + 2) * V * RS, 0);

@@ -5,6 +5,7 @@
 // -fsanitize=address,undefined).
 #pragma once
 
+#include <climits>
 #include <cstdint>
 #include <string>
 #include <vector>
@@ -27,11 +28,20 @@ struct I4 {
 //   [2 + 3*(L-2) + 0]       bo(c_L) as float bits      (L = 2..m)
 //   [2 + 3*(L-2) + 1]       first arc of c_L (index into arcs)
 //   [2 + 3*(L-2) + 2]       number of arcs of c_L
+//   [record_ctx_word(N)]    deepest level D >= 2 of the chain whose context
+//                           has a context row, and that row: D << 28 | row
+//                           (0: none)
 // (a one-token state w has m = 1 and no level entries)
-inline int record_stride(int N) {
-  int w = 2 + 3 * (N > 2 ? N - 2 : 0);
-  return (w + 3) & ~3;  // 16-byte records
-}
+inline int record_ctx_word(int N) { return 2 + 3 * (N > 2 ? N - 2 : 0); }
+inline int record_stride(int N) { return (record_ctx_word(N) + 1 + 3) & ~3; }  // 16-byte records
+
+// A context of L >= 2 tokens gets a context row when it has more than
+// context_row_min_arcs(N) explicit successors: then the successors of the
+// levels above the deepest such context of any state, at most N-2 levels,
+// number at most 1024 in total.  The environment variable
+// FUSION_CONTEXT_ROW_MIN_ARCS, read at each load, replaces the threshold
+// (tests lower it to give small models context rows).
+int64_t context_row_min_arcs(int N);
 
 // The n-gram model laid out for the fusion kernels (see LMDevice for the
 // meaning of each array).
@@ -44,6 +54,13 @@ struct LMHost {
   std::vector<float> dense, eos1;
   std::vector<int32_t> rec_dense, cnt1, rec, top_next;
   std::vector<I2> arcs;
+  // context rows: ctx_lm[r * V + y] = lm(y | c) for the r-th context c with a
+  // row (the backoff recursion's own fp32 value), ctx_rec[(r * V + y) * RS]
+  // the record of the state after (c, y) when no longer context than c has
+  // an arc for y
+  int64_t n_ctx = 0;
+  std::vector<float> ctx_lm;
+  std::vector<int32_t> ctx_rec;
 };
 
 // ngram_load's arguments (see fusion.h) -> *out; FUSION_OK or an error code

@@ -3,6 +3,8 @@
 // n-gram model and a phrase list in a plain binary form (little-endian; see
 // write_case in the test), builds both host layouts and prints their sizes
 // and a checksum of every array, or the error code the builders return.
+// With a second argument it also writes the state records, the context rows
+// and the level-1 next-state records there.
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -40,7 +42,7 @@ uint64_t sum_bytes(const std::vector<T> &v) {
 }  // namespace
 
 int main(int argc, char **argv) {
-  if (argc != 2) return 2;
+  if (argc != 2 && argc != 3) return 2;
   g_in = fopen(argv[1], "rb");
   if (!g_in) return 2;
   const int32_t N = read_one<int32_t>(), V = read_one<int32_t>(), blank = read_one<int32_t>();
@@ -79,6 +81,17 @@ int main(int argc, char **argv) {
            (unsigned long long)sum_bytes(lm.rec_dense), (unsigned long long)sum_bytes(lm.cnt1),
            (unsigned long long)sum_bytes(lm.eos1), (unsigned long long)sum_bytes(lm.rec),
            (unsigned long long)sum_bytes(lm.arcs), (unsigned long long)sum_bytes(lm.top_next));
+    printf("lm_ctx n_ctx=%lld\n", (long long)lm.n_ctx);
+    if (argc == 3) {  // the records and context rows, for the test to check against the oracle
+      FILE *f = fopen(argv[2], "wb");
+      const int64_t hdr[4] = {lm.rec_stride, lm.n_ctx, (int64_t)lm.rec.size(), (int64_t)lm.rec_dense.size()};
+      fwrite(hdr, sizeof hdr, 1, f);
+      fwrite(lm.rec.data(), 4, lm.rec.size(), f);
+      fwrite(lm.ctx_lm.data(), 4, lm.ctx_lm.size(), f);
+      fwrite(lm.ctx_rec.data(), 4, lm.ctx_rec.size(), f);
+      fwrite(lm.rec_dense.data(), 4, lm.rec_dense.size(), f);
+      fclose(f);
+    }
   }
   fusion::TrieHost tr;
   rc = fusion::build_trie_host(V, blank, n_ph, ptok.data(), offs.data(), has_comp ? comp.data() : nullptr, ts, &tr,

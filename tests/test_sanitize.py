@@ -106,3 +106,54 @@ def test_oracle_pins_under_sanitizers(tmp_path):
                         *tests], capture_output=True, text=True, env=env, cwd=ROOT, timeout=900)
     assert r.returncode == 0 and "ERROR: AddressSanitizer" not in r.stderr + r.stdout \
         and "runtime error" not in r.stderr + r.stdout, (r.stdout[-3000:], r.stderr[-3000:])
+
+
+@pytest.mark.parametrize("seed,N,X", [(0, 4, 3), (1, 5, 2), (2, 6, 4), (3, 3, 5)])
+def test_context_rows_equal_the_backoff_recursion(driver, tmp_path, seed, N, X):
+    """With the threshold lowered (FUSION_CONTEXT_ROW_MIN_ARCS), every context
+    of 2..N-1 tokens with more than X successors gets a row.  Each row entry
+    must be the oracle's fp32 backoff recursion lm(y | c) bit for bit, each
+    next-state record the oracle's state after c y (its longest present
+    suffix), and each state record must name the deepest context of its chain
+    that has a row."""
+    import oracle
+
+    rng = np.random.default_rng(950 + seed)
+    V = 23
+    lm = tiny_random_lm(rng, V, N, n_sent=400, cutoffs=tuple([1] * N))
+    ph = tiny_random_phrases(rng, V, n=3, max_len=3)
+    path, dump = str(tmp_path / "lm.bin"), str(tmp_path / "lm.dump")
+    write_case(path, lm, ph)
+    env = dict(ENV, FUSION_CONTEXT_ROW_MIN_ARCS=str(X))
+    r = subprocess.run([driver, path, dump], capture_output=True, text=True, env=env, timeout=600)
+    assert r.returncode == 0 and "runtime error" not in r.stderr, r.stderr[-2000:]
+    olm = oracle.OracleLM(lm)
+    # the contexts with rows, in row order: by length, then lexicographically
+    ctxs = []
+    for L in range(2, N):
+        rows = [tuple(int(v) for v in t) for t in lm.tokens[L - 1]]
+        nxt = [tuple(int(v) for v in t) for t in lm.tokens[L]]
+        for c in sorted(rows):
+            if sum(1 for t in nxt if t[:L] == c) > X:
+                ctxs.append(c)
+    with open(dump, "rb") as f:
+        RS, n_ctx, n_rec, _ = (int(v) for v in np.frombuffer(f.read(32), np.int64))
+        rec = np.frombuffer(f.read(4 * n_rec), np.int32).reshape(-1, RS)
+        ctx_lm = np.frombuffer(f.read(4 * n_ctx * V), np.float32).reshape(n_ctx, V)
+        ctx_rec = np.frombuffer(f.read(4 * n_ctx * V * RS), np.int32).reshape(n_ctx, V, RS)
+    assert n_ctx == len(ctxs) and n_ctx > 0, (n_ctx, len(ctxs))
+    for r_, c in enumerate(ctxs):
+        for y in range(1, V):
+            assert ctx_lm[r_, y] == olm.logp32(list(c), y), (c, y)
+            assert ctx_rec[r_, y, 1] == olm.state_of_history(list(c) + [y]), (c, y)
+    # state records: the deepest context of the chain with a row
+    cw = 2 + 3 * (N - 2)
+    index = {c: i for i, c in enumerate(ctxs)}
+    for sid in range(V + 2, V + 2 + rec.shape[0]):
+        t = olm.state_tuple(sid)
+        want = 0
+        for L in range(len(t), 1, -1):
+            if t[-L:] in index:
+                want = (L << 28) | index[t[-L:]]
+                break
+        assert rec[sid - V - 2, cw] == want, (t, rec[sid - V - 2, cw], want)
