@@ -252,6 +252,29 @@ int fusion_run_lms(const NgramTables *const *lms, const float *alphas, int32_t n
                    hipStream_t stream);
 
 /*
+ * fusion_run_lms_noalloc - fusion_run_lms for callers that cannot allocate
+ * device memory: code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc.  Same arguments, results and errors as
+ * fusion_run_lms; it calls no hipMalloc / hipFree / allocating routine.  The
+ * beam's exchange records (B > 1) live in a library-owned static device array
+ * of FUSION_NOALLOC_SCRATCH_BYTES on each GPU, held until the process ends;
+ * streams that do not fit in it at once run in further launches.  One
+ * stream's records (2 * B * k * (3 + n_lm + recombine) 8-byte words) must fit
+ * (FUSION_E_UNSUPPORTED otherwise; every size within this build's limits
+ * does).  Every call on a GPU shares that GPU's array and leaves the last
+ * call's records in it (each launch clears what it uses first): calls that
+ * overlap on one GPU, on different streams or threads, race and must not be
+ * made.  Greedy calls (B == 1) use no scratch at all.
+ */
+#define FUSION_NOALLOC_SCRATCH_BYTES (1 << 20)
+int fusion_run_lms_noalloc(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
+                           const BoostTrie *trie, const float *logits, int32_t T, int32_t S, int32_t B,
+                           int32_t V, int32_t k, float beta, int32_t blank_id, int32_t blank_mode,
+                           int32_t *lm_state, int32_t *boost_state, double *hyp_score, int32_t *tokens,
+                           int32_t *parents, float *fused, int64_t *traffic, int32_t flags, uint64_t *hist,
+                           hipStream_t stream);
+
+/*
  * fusion_end_scores - end-of-stream scoring: the LM terms of Eq. (1) for the
  * end-of-sentence token </s>, added when a stream ends so that its hypotheses
  * are compared as complete sentences.

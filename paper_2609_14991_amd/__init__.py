@@ -38,6 +38,7 @@ FUSION_RUN_RECOMBINE = 1
 
 EXPORTS = ("ngram_load", "ngram_bos_state", "ngram_info", "ngram_free", "boost_build", "boost_info",
            "boost_free", "fusion_step", "fusion_run", "fusion_step_lms", "fusion_run_lms",
+           "fusion_run_lms_noalloc",
            "fusion_end_scores", "joint_project", "fusion_last_error", "fusion_device_status")
 
 
@@ -86,6 +87,8 @@ def lib():
         L.fusion_run_lms.restype = ctypes.c_int
         L.fusion_run_lms.argtypes = [vp, vp, i32, vp, vp, i32, i32, i32, i32, i32, f32, i32, i32, vp,
                                      vp, vp, vp, vp, vp, vp, i32, vp, vp]
+        L.fusion_run_lms_noalloc.restype = ctypes.c_int
+        L.fusion_run_lms_noalloc.argtypes = L.fusion_run_lms.argtypes
         L.fusion_end_scores.restype = ctypes.c_int
         L.fusion_end_scores.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp]
         L.joint_project.restype = ctypes.c_int
@@ -293,6 +296,19 @@ def fusion_run_lms(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, bla
                                 int(blank_mode), _ptr(lm_state), _ptr(boost_state), _ptr(hyp_score),
                                 _ptr(tokens), _ptr(parents), _ptr(fused), _ptr(traffic), int(flags),
                                 _ptr(hist), _stream(stream)))
+
+
+def fusion_run_lms_noalloc(lms, alphas, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
+                           boost_state, hyp_score, tokens, parents, fused=None, traffic=None, flags=0, hist=None,
+                           stream=None):
+    """fusion_run_lms through the entry point that allocates no device memory
+    (its beam exchange lives in the library's static per-GPU scratch)."""
+    hs, al, n = _lm_arrays(lms, alphas)
+    _check(lib().fusion_run_lms_noalloc(ctypes.cast(hs, ctypes.c_void_p), _ptr(al), n, _h(trie), _ptr(logits),
+                                        int(T), int(S), int(B), int(V), int(k), float(beta), int(blank_id),
+                                        int(blank_mode), _ptr(lm_state), _ptr(boost_state), _ptr(hyp_score),
+                                        _ptr(tokens), _ptr(parents), _ptr(fused), _ptr(traffic), int(flags),
+                                        _ptr(hist), _stream(stream)))
 
 
 def fusion_end_scores(lms, alphas, lm_state, H, hyp_score=None, end_term=None, stream=None):

@@ -62,6 +62,13 @@ constexpr int kSpinLimit = 1 << 20;           // bounded wait at the beam rendez
 __device__ int g_status;
 __device__ int32_t g_zero_words[4];  // never written: read by lanes that have no record word
 
+// Beam exchange memory of fusion_run_lms_noalloc, one copy per GPU, held until
+// the process ends.  Host code never passes this name to a kernel: it is a
+// host-side stand-in, not a device address.  The device address comes from
+// hipGetSymbolAddress (static_scratch below) and is what the kernels receive.
+constexpr size_t kStaticScratchBytes = FUSION_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned long long scratch[kStaticScratchBytes / sizeof(unsigned long long)];
+
 struct Params {
   LMDevice lm[FUSION_MAX_LMS];  // the n_lm models of Eq. (1), each with its own weight lam[i]
   TrieDevice tr;
@@ -1477,7 +1484,29 @@ DeviceInfo device_info() {
   return cache[dev];
 }
 
-int launch(Params &p, int n_hyp, hipStream_t stream) {
+// The device address of this GPU's static scratch array, looked up once per
+// device (with that device current) and kept; nullptr after a failed lookup.
+int static_scratch(unsigned long long **out) {
+  static std::mutex mu;
+  static unsigned long long *ptr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_error(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) return set_error(FUSION_E_UNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lk(mu);
+  if (!ptr[dev]) {
+    void *a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_error(e, "hipGetSymbolAddress(scratch)");
+    ptr[dev] = reinterpret_cast<unsigned long long *>(a);
+  }
+  *out = ptr[dev];
+  return FUSION_OK;
+}
+
+// fixed: caller-provided exchange memory of fixed_words 64-bit words (no
+// allocation); nullptr: the exchange is allocated stream-ordered per call
+int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed = nullptr, size_t fixed_words = 0) {
   const Shape sh = shape_for(p.V);
   const int km = p.k <= 1 ? 1 : p.k <= 4 ? 4 : 8;
   const bool al = (p.V % 4 == 0) && ((uintptr_t)p.logits % 16 == 0) && (!p.fused || (uintptr_t)p.fused % 16 == 0);
@@ -1510,12 +1539,19 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
   int s_batch = (int)std::min<long>(p.S, resident / p.B);
   // exchange records: 2 buffers x B x k candidates x (3 + n_lm (+1 recombining)) words per stream
   const size_t stream_words = (size_t)2 * p.B * p.k * (3 + p.n_lm + (p.recombine ? 1 : 0));
+  if (fixed) {
+    if (stream_words > fixed_words)
+      return set_error(FUSION_E_UNSUPPORTED, "one stream's beam exchange exceeds the static scratch");
+    s_batch = (int)std::min<size_t>((size_t)s_batch, fixed_words / stream_words);
+  }
   if (s_batch >= 8) s_batch -= s_batch % 8;
   if (s_batch < 1) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device at once");
   const size_t xwords = (size_t)s_batch * stream_words;
-  void *xbuf = nullptr;
-  e = hipMallocAsync(&xbuf, xwords * sizeof(unsigned long long), stream);
-  if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
+  void *xbuf = fixed;
+  if (!fixed) {
+    e = hipMallocAsync(&xbuf, xwords * sizeof(unsigned long long), stream);
+    if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
+  }
   p.xchg = reinterpret_cast<unsigned long long *>(xbuf);
   int rc = FUSION_OK;
   for (int s0 = 0; s0 < p.S && rc == FUSION_OK; s0 += s_batch) {
@@ -1537,8 +1573,10 @@ int launch(Params &p, int n_hyp, hipStream_t stream) {
     e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(ns * p.B), dim3(sh.W), args, dyn, stream);
     if (e != hipSuccess) rc = hip_error(e, "cooperative fusion kernel launch");
   }
-  hipError_t e2 = hipFreeAsync(xbuf, stream);
-  if (rc == FUSION_OK && e2 != hipSuccess) rc = hip_error(e2, "hipFreeAsync");
+  if (!fixed) {
+    hipError_t e2 = hipFreeAsync(xbuf, stream);
+    if (rc == FUSION_OK && e2 != hipSuccess) rc = hip_error(e2, "hipFreeAsync");
+  }
   return rc;
 }
 
@@ -1611,7 +1649,7 @@ int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, c
              const float *logits, int32_t T, int32_t S, int32_t B, int32_t V, int32_t k, float beta,
              int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state, double *hyp_score,
              int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, int32_t flags, uint64_t *hist,
-             hipStream_t stream) {
+             hipStream_t stream, bool no_alloc = false) {
   int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta, T != 0 && S != 0);
   if (rc != FUSION_OK) return rc;
   if (T < 0 || S < 0 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
@@ -1642,6 +1680,12 @@ int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, c
   p.beta = beta;
   p.recombine = (flags & FUSION_RUN_RECOMBINE) && B > 1;
   p.hist = p.recombine ? reinterpret_cast<unsigned long long *>(hist) : nullptr;
+  if (no_alloc) {
+    unsigned long long *xs = nullptr;
+    rc = static_scratch(&xs);
+    if (rc != FUSION_OK) return rc;
+    return launch(p, S * B, stream, xs, kStaticScratchBytes / sizeof(unsigned long long));
+  }
   return launch(p, S * B, stream);
 }
 
@@ -1704,4 +1748,14 @@ extern "C" int fusion_run_lms(const NgramTables *const *lms, const float *alphas
                               uint64_t *hist, hipStream_t stream) {
   return run_impl(lms, alphas, n_lm, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
                   boost_state, hyp_score, tokens, parents, fused, traffic, flags, hist, stream);
+}
+
+extern "C" int fusion_run_lms_noalloc(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
+                                      const BoostTrie *trie, const float *logits, int32_t T, int32_t S,
+                                      int32_t B, int32_t V, int32_t k, float beta, int32_t blank_id,
+                                      int32_t blank_mode, int32_t *lm_state, int32_t *boost_state,
+                                      double *hyp_score, int32_t *tokens, int32_t *parents, float *fused,
+                                      int64_t *traffic, int32_t flags, uint64_t *hist, hipStream_t stream) {
+  return run_impl(lms, alphas, n_lm, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
+                  boost_state, hyp_score, tokens, parents, fused, traffic, flags, hist, stream, true);
 }
