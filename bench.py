@@ -46,7 +46,8 @@ def log(msg):
 # sources that decide what the fusion kernel reads and writes; the HBM traffic
 # recorded under profiles/ is reported only while they are unchanged
 KERNEL_SOURCES = ("paper_2609_14991_amd/csrc/fusion_kernels.hip", "paper_2609_14991_amd/csrc/fusion_internal.h",
-                  "paper_2609_14991_amd/csrc/ngram_tables.cpp", "paper_2609_14991_amd/csrc/boost_trie.cpp")
+                  "paper_2609_14991_amd/csrc/ngram_tables.cpp", "paper_2609_14991_amd/csrc/boost_trie.cpp",
+                  "paper_2609_14991_amd/csrc/tables_host.cpp", "paper_2609_14991_amd/csrc/tables_host.h")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fusion_kernel_c5_hbm_traffic.md")
 TRAFFIC_FILE_TWO_LMS = os.path.join(ROOT, "profiles", "fusion_kernel_c5_two_lms_hbm_traffic.md")
 TRAFFIC_FILE_RC = os.path.join(ROOT, "profiles", "fusion_kernel_c5_recombining_hbm_traffic.md")
