@@ -266,7 +266,7 @@ def keyword_leg(F, torch, dev, stream, n_launch):
     }
 
 
-def projection_leg(F, torch, dev, stream, cfg):
+def projection_leg(F, torch, dev, stream, cfg, w=None, lm=None, trie=None):
     """The joint output projection (bf16 MFMA) that would produce C5's logits:
     the per-frame shape [256, 640] x [640, 4096] (one frame of all hypotheses)
     and the batch of all 300 frames [76800, 640] x [640, 4096], each timed with
@@ -302,8 +302,68 @@ def projection_leg(F, torch, dev, stream, cfg):
             "min_hbm_bytes": pbytes, "hbm_gbs_at_min_bytes": pbytes / (pms / 1e3) / 1e9,
         }
         log(f"joint projection {m}x{N}x{K}: {pms * 1e3:.1f} us, {flops / (pms / 1e3) / 1e12:.1f} TFLOP/s")
+    if w is not None:
+        out["producer_loop"] = producer_leg(F, torch, dev, stream, w, lm, trie, a_d, w_d, b_d, o_d, K)
     del a_d, w_d, b_d, o_d
     return out
+
+
+def producer_leg(F, torch, dev, stream, w, lm, trie, a_d, w_d, b_d, o_d, K, n_launch=5):
+    """C5 decoded with the joint projection as the producer of its logits:
+    fusion_run_projected per frame (chunk 1: the [256, 640] x [640, 4096]
+    projection, then the frame's fusion step), per 13-frame chunk (a streaming
+    encoder chunk) and over all 300 frames at once, against the batched order
+    (one joint_project of all frames, then one fusion_run), each timed end to
+    end with HIP events; every decode's decisions must equal the batched one's."""
+    T, S, B, V, k, H = w.T, w.S, w.B, w.V, w.k, w.H
+    bos = F.ngram_bos_state(lm)
+    sc0 = torch.from_numpy(np.tile(np.array([0.0] + [-np.inf] * (B - 1)), S)).to(dev)
+    mode = F.FUSION_BLANK_COMPETE
+    runs = {"chunk_1": 1, "chunk_13": 13, f"chunk_{T}": T, "batched": None}
+    st = {n: (torch.empty((H,), dtype=torch.int32, device=dev), torch.empty((H,), dtype=torch.int32, device=dev),
+              torch.empty((H,), dtype=torch.float64, device=dev),
+              torch.empty((T, H), dtype=torch.int32, device=dev), torch.empty((T, H), dtype=torch.int32, device=dev))
+          for n in runs}
+
+    def reset(n):
+        ls, bs, sc = st[n][:3]
+        ls.fill_(bos)
+        bs.zero_()
+        sc.copy_(sc0)
+
+    def run(n):
+        ls, bs, sc, tok, par = st[n]
+        if runs[n] is None:
+            F.joint_project(a_d, w_d, b_d, T * H, V, K, o_d, stream.cuda_stream)
+            F.fusion_run(lm, trie, o_d, T, S, B, V, k, w.lam, w.beta, w.blank, mode, ls, bs, sc, tok, par, None, None,
+                         stream.cuda_stream)
+        else:
+            F.fusion_run_projected([lm], [w.lam], trie, a_d, w_d, b_d, K, o_d, runs[n], T, S, B, V, k, w.beta,
+                                   w.blank, mode, ls, bs, sc, tok, par, stream=stream.cuda_stream)
+
+    res = {}
+    for name in runs:
+        for _ in range(2):
+            reset(name)
+            run(name)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_launch)]
+        torch.cuda.synchronize()
+        for a, b in ev:
+            reset(name)
+            a.record(stream)
+            run(name)
+            b.record(stream)
+        torch.cuda.synchronize()
+        ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+        res[name] = {"frames_per_projection": runs[name] or T, "ms": ms, "us_per_frame": ms * 1e3 / T}
+    assert F.fusion_device_status() == 0
+    same = all(torch.equal(x, y) for n in runs for x, y in zip(st[n], st["batched"]))
+    res["decisions_equal"] = bool(same)
+    res["note"] = ("chunk_c: fusion_run_projected with c frames per projection ([c*H, K] x [K, V] into a [c, H, V] "
+                   "workspace, then one decode launch of those c frames); batched: one [T*H, K] x [K, V] projection "
+                   "then one fusion_run; each launch of a beam decode is cooperative (a fixed cost per launch)")
+    log("producer loop (C5): " + ", ".join(f"{n} {res[n]['ms']:.3f} ms" for n in runs) + f", decisions equal {same}")
+    return res
 
 
 def step_leg(F, torch, dev, stream, w, lm, trie, x, n_calls=300):
@@ -538,7 +598,7 @@ def main():
     out["fusion_step"] = step_leg(F, torch, dev, stream, w, lm, trie, x)
 
     if not args.no_projection:
-        out["projection"] = projection_leg(F, torch, dev, stream, args.config)
+        out["projection"] = projection_leg(F, torch, dev, stream, args.config, w, lm, trie)
 
     # Eq. (1) with two LMs: the same decode with a second, keyword 4-gram LM
     # (weights lambda, lambda), timed the same way; not part of the step above

@@ -312,6 +312,33 @@ int fusion_end_scores(const NgramTables *const *lms, const float *alphas, int32_
 int joint_project(const uint16_t *A, const uint16_t *W, const float *bias, int32_t M, int32_t N,
                   int32_t K, float *out, hipStream_t stream);
 
+/*
+ * fusion_run_projected - the frame loop with the joint output projection as its
+ * producer (the joint network's output layer feeds the acoustic term of Eq. (1),
+ * Sec. III): frames are taken in chunks of `chunk` frames (the last may be
+ * shorter); for each chunk, joint_project turns the chunk's joint hidden states
+ * into logits [chunk, H, V] in the caller's workspace, and the chunk's frames
+ * are decoded by fusion_run_lms (states, scores and history hashes carried to
+ * the next chunk), all enqueued on `stream`.  chunk = 1 is the per-frame
+ * producer; a streaming recogniser passes the frames of one encoder chunk.
+ *   A        device [T, H, K] bf16: joint hidden states, frame-major
+ *   W, bias  device [V, K] bf16 and [V] fp32 or NULL, as in joint_project
+ *   logits   device [chunk, H, V] fp32 workspace (holds the last chunk's
+ *            logits on return, at its first rows)
+ *   chunk    frames per projection, 1 <= chunk (larger than T acts as T)
+ * Every other argument is as in fusion_run_lms (no fused rows, no traffic
+ * count).  The results equal joint_project over all T * H rows followed by one
+ * fusion_run_lms over the T frames, bit for bit, for every chunk size.  With a
+ * beam the exchange records live through all chunks (allocated once per call,
+ * stream-ordered), and the frames of every chunk after the first are numbered
+ * on from the previous chunk's, so the records need no reset between chunks.
+ */
+int fusion_run_projected(const NgramTables *const *lms, const float *alphas, int32_t n_lm, const BoostTrie *trie,
+                         const uint16_t *A, const uint16_t *W, const float *bias, int32_t K, float *logits,
+                         int32_t chunk, int32_t T, int32_t S, int32_t B, int32_t V, int32_t k, float beta, int32_t blank_id,
+                         int32_t blank_mode, int32_t *lm_state, int32_t *boost_state, double *hyp_score,
+                         int32_t *tokens, int32_t *parents, int32_t flags, uint64_t *hist, hipStream_t stream);
+
 /* description of the calling thread's last failure (library-owned string) */
 const char *fusion_last_error(void);
 /* synchronizes `stream`, returns the device status bits in *code and clears them */

@@ -38,7 +38,7 @@ FUSION_RUN_RECOMBINE = 1
 
 EXPORTS = ("ngram_load", "ngram_bos_state", "ngram_info", "ngram_free", "boost_build", "boost_info",
            "boost_free", "fusion_step", "fusion_run", "fusion_step_lms", "fusion_run_lms",
-           "fusion_run_lms_noalloc",
+           "fusion_run_lms_noalloc", "fusion_run_projected",
            "fusion_end_scores", "joint_project", "fusion_last_error", "fusion_device_status")
 
 
@@ -89,6 +89,9 @@ def lib():
                                      vp, vp, vp, vp, vp, vp, i32, vp, vp]
         L.fusion_run_lms_noalloc.restype = ctypes.c_int
         L.fusion_run_lms_noalloc.argtypes = L.fusion_run_lms.argtypes
+        L.fusion_run_projected.restype = ctypes.c_int
+        L.fusion_run_projected.argtypes = [vp, vp, i32, vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, i32, i32, f32, i32,
+                                           i32, vp, vp, vp, vp, vp, i32, vp, vp]
         L.fusion_end_scores.restype = ctypes.c_int
         L.fusion_end_scores.argtypes = [vp, vp, i32, vp, i32, vp, vp, vp]
         L.joint_project.restype = ctypes.c_int
@@ -309,6 +312,18 @@ def fusion_run_lms_noalloc(lms, alphas, trie, logits, T, S, B, V, k, beta, blank
                                         int(blank_mode), _ptr(lm_state), _ptr(boost_state), _ptr(hyp_score),
                                         _ptr(tokens), _ptr(parents), _ptr(fused), _ptr(traffic), int(flags),
                                         _ptr(hist), _stream(stream)))
+
+
+def fusion_run_projected(lms, alphas, trie, A, W, bias, K, logits, chunk, T, S, B, V, k, beta, blank_id, blank_mode,
+                         lm_state, boost_state, hyp_score, tokens, parents, flags=0, hist=None, stream=None):
+    """Same arguments as the C call: A [T, S*B, K] and W [V, K] bf16 (int16 bit
+    patterns), logits a [chunk, S*B, V] float32 workspace; CUDA (HIP) tensors."""
+    hs, al, n = _lm_arrays(lms, alphas)
+    _check(lib().fusion_run_projected(ctypes.cast(hs, ctypes.c_void_p), _ptr(al), n, _h(trie), _ptr(A), _ptr(W),
+                                      _ptr(bias), int(K), _ptr(logits), int(chunk), int(T), int(S), int(B), int(V), int(k),
+                                      float(beta), int(blank_id), int(blank_mode), _ptr(lm_state), _ptr(boost_state),
+                                      _ptr(hyp_score), _ptr(tokens), _ptr(parents), int(flags), _ptr(hist),
+                                      _stream(stream)))
 
 
 def fusion_end_scores(lms, alphas, lm_state, H, hyp_score=None, end_term=None, stream=None):

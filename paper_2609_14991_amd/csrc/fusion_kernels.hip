@@ -34,6 +34,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "fusion_internal.h"
 
@@ -55,12 +56,11 @@ namespace {
 constexpr int kMaxWaves = 16;
 constexpr int kMaxLevels = FUSION_MAX_ORDER;  // context levels 1..N-1 <= 5
 constexpr int kAux = 256;                     // LDS side tables: phrase transitions, top-level next states
-constexpr int kNodeLane = 32;                 // lanes 32..35 of the record word hold the phrase node
-constexpr int kLM1Lane = 40;                  // lanes 40..59 hold the second LM's record
+constexpr int kRecW = 16;                     // words read per state record: record_stride(FUSION_MAX_ORDER)
 constexpr int kSpinLimit = 1 << 20;           // bounded wait at the beam rendezvous (polls, ~1 s)
 
 __device__ int g_status;
-__device__ int32_t g_zero_words[4];  // never written: read by lanes that have no record word
+__device__ __align__(64) int32_t g_zero_words[16];  // never written: the record and node of "no state"
 
 // Beam exchange memory of fusion_run_lms_noalloc, one copy per GPU, held until
 // the process ends.  Host code never passes this name to a kernel: it is a
@@ -85,7 +85,9 @@ struct Params {
   int32_t *next_boost;
   unsigned long long *xchg;  // beam exchange [S][2][B][k] candidate records of four tagged words
   unsigned long long *hist;  // recombination: [H] in/out history hashes (0: derive from the initial states) or NULL
-  int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, n_lm, recombine, pad;
+  // t_base: the number of frames decoded by earlier calls of a frame loop that
+  // keeps the exchange between calls (its records are tagged by global frame)
+  int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, n_lm, recombine, t_base;
   float lam[FUSION_MAX_LMS], beta;
 };
 
@@ -94,7 +96,6 @@ __device__ __forceinline__ bool before(float ka, int ya, float kb, int yb) {
 }
 __device__ __forceinline__ float as_float(int v) { return __int_as_float(v); }
 __device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
-__device__ __forceinline__ int rdl(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 // the splitmix64 finalizer: a 64-bit mix for the beam's history hashes
 __device__ __forceinline__ unsigned long long mix64(unsigned long long z) {
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
@@ -138,11 +139,11 @@ __device__ __forceinline__ void row_store1(rsrc_t r, float v, int voff, int soff
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
 // record words: [0] c_1 | m << 16, [1] state id, [2 + 3(L-2) + {0,1,2}] = (bo, first arc, arcs) of level L
-__device__ __forceinline__ int rec_bo_lane(int L) { return 2 + 3 * (L - 2); }
-__device__ __forceinline__ int rec_beg_lane(int L) { return 3 + 3 * (L - 2); }
-__device__ __forceinline__ int rec_cnt_lane(int L) { return 4 + 3 * (L - 2); }
+__device__ __forceinline__ constexpr int rec_bo_word(int L) { return 2 + 3 * (L - 2); }
+__device__ __forceinline__ constexpr int rec_beg_word(int L) { return 3 + 3 * (L - 2); }
+__device__ __forceinline__ constexpr int rec_cnt_word(int L) { return 4 + 3 * (L - 2); }
 // the record word naming the chain's context row (record_ctx_word)
-__device__ __forceinline__ int rec_ctx_lane(int N) { return 2 + 3 * (N > 2 ? N - 2 : 0); }
+__device__ __forceinline__ constexpr int rec_ctx_word(int N) { return 2 + 3 * (N > 2 ? N - 2 : 0); }
 
 // ---- wave-level reductions with DPP moves (no LDS) ------------------------------
 // rows of 16 lanes: quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror,
@@ -247,8 +248,6 @@ struct HypState {
   unsigned long long hist;  // 48-bit hash of the history (initial states, emitted tokens): recombination
 };
 
-// first lane of LM i's record in the record word
-__device__ __forceinline__ constexpr int rec_lane0(int i) { return i == 0 ? 0 : kLM1Lane; }
 
 // MODE: what a launch computes (the code of the other modes is compiled out)
 // (kModeBeamRC: beam with recombination of equal histories)
@@ -547,56 +546,55 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j) xv[c][j] = (act && (c * W + g) * 4 + j < V) ? xraw[c][j] : -INFINITY;
-    // lanes 0..RS-1: record words of the first LM; lanes 32..35: phrase node;
-    // lanes 40..40+RS-1: record words of the second LM; every other lane, and
-    // every lane without a record or node, reads a zero word.  One load per lane,
-    // used as loaded, so that decoding the records waits for them alone and not
-    // for the dense rows and the logits fetched after them
-    int rw;
-    {
-      const int32_t *src = &g_zero_words[0];
-      if (rp[0] && lane < RSl[0]) src = rp[0] + lane;
-      if (np && lane >= kNodeLane && lane < kNodeLane + 4) src = reinterpret_cast<const int *>(np) + (lane - kNodeLane);
-      if (NL > 1 && rp[NL - 1] && lane >= kLM1Lane && lane < kLM1Lane + RSl[NL - 1])
-        src = rp[NL - 1] + (lane - kLM1Lane);
-      rw = *src;
+    // the state records and the phrase node with scalar loads (uniform addresses):
+    // kRecW words per record (the record arrays carry a tail pad so that reading
+    // past a short record stays inside them); "no record" / "no node" read the
+    // zero words
+    int rec[NL][kRecW];
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const __attribute__((address_space(4))) int32_t *r =
+          (const __attribute__((address_space(4))) int32_t *)(rp[i] ? rp[i] : g_zero_words);
+#pragma unroll
+      for (int w = 0; w < kRecW; ++w) rec[i][w] = r[w];
     }
+    const __attribute__((address_space(4))) int32_t *nq =
+        (const __attribute__((address_space(4))) int32_t *)(np ? reinterpret_cast<const int32_t *>(np) : g_zero_words);
+    const int node[4] = {nq[0], nq[1], nq[2], nq[3]};
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
       // the initial state of a run may need its record to learn c_1
-      if (ok && c1[i] < 0) c1[i] = rp[i] ? (rdl(rw, rec_lane0(i)) & 0xFFFF) : lmsrc[i];
+      if (ok && c1[i] < 0) c1[i] = rp[i] ? (rec[i][0] & 0xFFFF) : lmsrc[i];
       // level-1 dense row straight into the LM's LDS row.  Issued
       // unconditionally (row 0 stands in when the hypothesis has no keys to
-      // compute this frame), so that the record decode can wait for the record
-      // alone
+      // compute this frame), so that only the records are waited for before the
+      // second hop
       load_row(lms[i].dense + (int64_t)(ok ? c1[i] : 0) * V, lmval + i * Vp, V);
     }
     if (NW == 1 && t > 0) row_stats(xraw, 0, V);  // a single wave has no idle helper
     // ---- decode the records ---------------------------------------------------------
-    // (words a record does not use, the levels above m among them, read as 0, as do
-    // the node lanes without a node)
-    const float phiq = as_float(rdl(rw, kNodeLane));
-    const int dbeg = rdl(rw, kNodeLane + 1);
-    const int dcnt = rdl(rw, kNodeLane + 2);
-    const int qid = np ? rdl(rw, kNodeLane + 3) : qsrc;
+    const float phiq = as_float(node[0]);
+    const int dbeg = node[1];
+    const int dcnt = node[2];
+    const int qid = np ? node[3] : qsrc;
     // per LM: order m of the state, its id; backoffs, first arcs and arc counts of
-    // levels 2..7 as uniform values (readlane at fixed lanes is valid whatever
-    // the active mask); adding the zero backoffs above m changes no sum (at most
-    // the sign of a zero)
-    // The first LM's context row (level D >= 2 of the chain, row r) replaces the
-    // levels up to D: only the arcs of the levels above D are fetched (lcnt 0
-    // for the others).  Further LMs fetch the arcs of every level.
+    // levels 2..m.  The first LM's context row (level D >= 2 of the chain, row r)
+    // replaces the levels up to D: only the arcs of the levels above D are fetched
+    // (lcnt 0 for the others).  Further LMs fetch the arcs of every level.  The
+    // algorithmic bytes of the LM rows are counted here, over every level
     int m[NL], sid[NL], total_arcs[NL], Dc = 0, crow = 0;
     float bo[NL][kMaxLevels];
     int lcnt[NL][kMaxLevels], lbeg[NL][kMaxLevels];
+    unsigned long long lm_bytes = 0;
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
-      const int l0 = rec_lane0(i);
-      m[i] = rp[i] ? (rdl(rw, l0) >> 16) : 1;
-      sid[i] = rp[i] ? rdl(rw, l0 + 1) : lmsrc[i];
+      m[i] = rp[i] ? (rec[i][0] >> 16) : 1;
+      sid[i] = rp[i] ? rec[i][1] : lmsrc[i];
       int Di = 0;
       if (CTX && i == 0 && rp[0]) {
-        const int cw = rdl(rw, rec_ctx_lane(Nl[0]));
+        const int n0 = Nl[0];
+        const int cw = n0 == 3 ? rec[0][rec_ctx_word(3)] : n0 == 4 ? rec[0][rec_ctx_word(4)]
+                     : n0 == 5 ? rec[0][rec_ctx_word(5)] : n0 == 6 ? rec[0][rec_ctx_word(6)] : 0;
         Dc = Di = (int)((unsigned)cw >> 28);
         crow = cw & 0x0FFFFFFF;
       }
@@ -606,11 +604,13 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 #pragma unroll
       for (int L = 2; L < kMaxLevels; ++L) {
         const bool lv = L <= m[i];
-        bo[i][L] = lv ? as_float(rdl(rw, l0 + rec_bo_lane(L))) : 0.0f;
-        lcnt[i][L] = (lv && L > Di) ? rdl(rw, l0 + rec_cnt_lane(L)) : 0;
-        lbeg[i][L] = lv ? rdl(rw, l0 + rec_beg_lane(L)) : 0;
+        bo[i][L] = lv ? as_float(rec[i][rec_bo_word(L)]) : 0.0f;
+        lcnt[i][L] = (lv && L > Di) ? rec[i][rec_cnt_word(L)] : 0;
+        lbeg[i][L] = lv ? rec[i][rec_beg_word(L)] : 0;
         total_arcs[i] += lcnt[i][L];
+        if (lv) lm_bytes += umin64(8ull * (unsigned long long)(unsigned)rec[i][rec_cnt_word(L)], 4ull * V) + 12ull;
       }
+      if (m[i] >= 2) lm_bytes += 8ull;
     }
     if (CTX && ok && Dc >= 2) load_row(lms[0].ctx_lm + (int64_t)crow * V, lmval + NL * Vp, V);
     // ---- hop 2: first arcs of levels 2..m (flattened) and first phrase transitions --
@@ -624,16 +624,18 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         ab[i][u] = make_int2(INT_MAX, 0);
         at[i][u] = 0;
         tn[i][u] = 0;
-        // the level of flattened arc f: subtract the counts of the levels below
-        int L = 2, bL = lbeg[i][2];
+        // the level of flattened arc f against the (uniform) starts of the levels:
+        // the last level that starts at or before f; then f's offset within it
+        int L = 2, bL = lbeg[i][2], fo = f, e = 0;
 #pragma unroll
-        for (int L2 = 2; L2 < kMaxLevels - 1; ++L2) {
-          if (L2 >= m[i]) break;  // uniform: no arcs above m
-          const bool past = (L == L2) && (f >= lcnt[i][L2]);
-          f = past ? f - lcnt[i][L2] : f;
-          L = past ? L2 + 1 : L;
-          bL = past ? lbeg[i][L2 + 1] : bL;
+        for (int L2 = 3; L2 < kMaxLevels; ++L2) {
+          e += lcnt[i][L2 - 1];  // first flattened index of level L2
+          const bool past = f >= e && L2 <= m[i];
+          L = past ? L2 : L;
+          bL = past ? lbeg[i][L2] : bL;
+          fo = past ? f - e : fo;
         }
+        f = fo;
         if (u * W + g < total_arcs[i]) {
           at[i][u] = (L << 16) | f;
           ab[i][u] = lms[i].arcs[bL + f];
@@ -706,11 +708,12 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       // arcs beyond the first kUA * W of the flattened levels
 #pragma unroll
       for (int i = 0; i < NL; ++i) {
-        const int l0 = rec_lane0(i), N = Nl[i];
+        const int N = Nl[i];
         int covered = kUA * W;
-        for (int L = 2; L <= m[i]; ++L) {
-          const int bL = rdl(rw, l0 + rec_beg_lane(L));
-          const int cL = (i != 0 || L > Dc) ? rdl(rw, l0 + rec_cnt_lane(L)) : 0;
+#pragma unroll
+        for (int L = 2; L < kMaxLevels; ++L) {
+          if (L > m[i]) break;  // uniform
+          const int bL = lbeg[i][L], cL = lcnt[i][L];
           const int done = min(cL, max(0, covered));
           covered -= cL;
           const int2 *A = lms[i].arcs + bL;
@@ -820,10 +823,14 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         for (int i = 0; i < NL; ++i) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) dres[i][j] = lv[i][j];
-          for (int L2 = (CTX && i == 0 && Dc >= 2) ? Dc + 1 : 2; L2 <= m[i]; ++L2) {
-            const float b2 = as_float(rdl(rw, rec_lane0(i) + rec_bo_lane(L2)));
+          const int from = (CTX && i == 0 && Dc >= 2) ? Dc + 1 : 2;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) dres[i][j] = dres[i][j] + b2;
+          for (int L2 = 2; L2 < kMaxLevels; ++L2) {
+            if (L2 > m[i]) break;  // uniform
+            if (L2 >= from) {
+#pragma unroll
+              for (int j = 0; j < 4; ++j) dres[i][j] = dres[i][j] + bo[i][L2];
+            }
           }
         }
 #pragma unroll
@@ -995,12 +1002,8 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       if (ok) {
         const unsigned long long row = 4ull * V;
 #pragma unroll
-        for (int i = 0; i < NL; ++i) {
-          by += umin64(8ull * (unsigned long long)lms[i].cnt1[c1[i]], row);
-          for (int L2 = 2; L2 <= m[i]; ++L2)
-            by += umin64(8ull * (unsigned long long)rdl(rw, rec_lane0(i) + rec_cnt_lane(L2)), row) + 12ull;
-          if (m[i] >= 2) by += 8ull;
-        }
+        for (int i = 0; i < NL; ++i) by += umin64(8ull * (unsigned long long)lms[i].cnt1[c1[i]], row);
+        by += lm_bytes;
         if (p.has_trie) by += 16ull + 16ull * (unsigned long long)dcnt;
       }
       by += BEAM ? 8ull : 4ull;
@@ -1180,8 +1183,11 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         // one frame ahead of any reader of its stream, so it never overwrites a
         // buffer that is still being read.
         constexpr int XW = 3 + NL + (RC ? 1 : 0);
-        unsigned long long *xs = p.xchg + ((size_t)sl * 2 + (t & 1)) * (size_t)B * K * XW;
-        const unsigned long long tag = (unsigned long long)((t + 1) & 0xFFFF) << 48;
+        // tags run 1..65535 over the global frame index (0 marks a cleared record);
+        // a record left in a buffer is from two frames back, so never current
+        const int tg = p.t_base + t;
+        unsigned long long *xs = p.xchg + ((size_t)sl * 2 + (tg & 1)) * (size_t)B * K * XW;
+        const unsigned long long tag = (unsigned long long)(tg % 65535 + 1) << 48;
         constexpr unsigned long long kPay = (1ull << 48) - 1;
         if (lane < K) {
           const bool has = act && cy != INT_MAX;
@@ -1504,9 +1510,54 @@ int static_scratch(unsigned long long **out) {
   return FUSION_OK;
 }
 
+// Per device and kernel: its static LDS, resident workgroups per CU at the
+// launch's dynamic LDS, and whether that dynamic LDS has been granted; looked up
+// once (the dynamic LDS of a kernel is fixed by its template shape)
+struct KernelInfo {
+  const void *fn = nullptr;
+  int dev = -1;
+  size_t static_lds = 0;
+  int per_cu = 0;
+};
+
+int kernel_info(KernelFn fn, int W, size_t dyn, int lds_per_block, KernelInfo *out) {
+  static std::mutex mu;
+  static std::vector<KernelInfo> cache;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_error(e, "hipGetDevice");
+  const void *f = reinterpret_cast<const void *>(fn);
+  std::lock_guard<std::mutex> lk(mu);
+  for (const KernelInfo &ki : cache)
+    if (ki.fn == f && ki.dev == dev) {
+      *out = ki;
+      return FUSION_OK;
+    }
+  KernelInfo ki;
+  ki.fn = f;
+  ki.dev = dev;
+  hipFuncAttributes attr;
+  e = hipFuncGetAttributes(&attr, f);
+  if (e != hipSuccess) return hip_error(e, "hipFuncGetAttributes");
+  ki.static_lds = attr.sharedSizeBytes;
+  if (dyn + ki.static_lds > (size_t)lds_per_block)
+    return set_error(FUSION_E_UNSUPPORTED, "vocabulary too large for the device's LDS");
+  e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+  if (e != hipSuccess) return hip_error(e, "hipFuncSetAttribute");
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&ki.per_cu, f, W, dyn);
+  if (e != hipSuccess) return hip_error(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
+  cache.push_back(ki);
+  *out = ki;
+  return FUSION_OK;
+}
+
 // fixed: caller-provided exchange memory of fixed_words 64-bit words (no
-// allocation); nullptr: the exchange is allocated stream-ordered per call
-int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed = nullptr, size_t fixed_words = 0) {
+// allocation); nullptr: the exchange is allocated stream-ordered per call.
+// keep_exchange: the call continues a frame loop whose earlier calls used the
+// same exchange with p.t_base counting their frames, so its records need no
+// reset (only when one launch holds every stream; otherwise it is reset anyway)
+int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed = nullptr, size_t fixed_words = 0,
+           bool keep_exchange = false) {
   const Shape sh = shape_for(p.V);
   const int km = p.k <= 1 ? 1 : p.k <= 4 ? 4 : 8;
   const bool al = (p.V % 4 == 0) && ((uintptr_t)p.logits % 16 == 0) && (!p.fused || (uintptr_t)p.fused % 16 == 0);
@@ -1516,13 +1567,10 @@ int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed =
   const DeviceInfo di = device_info();
   if (!di.ok) return set_error(FUSION_E_HIP, "cannot query the device");
   const size_t dyn = dyn_lds_bytes(sh.Vp, p.n_lm);
-  hipFuncAttributes attr;
-  hipError_t e = hipFuncGetAttributes(&attr, reinterpret_cast<const void *>(fn));
-  if (e != hipSuccess) return hip_error(e, "hipFuncGetAttributes");
-  if (dyn + attr.sharedSizeBytes > (size_t)di.lds_per_block)
-    return set_error(FUSION_E_UNSUPPORTED, "vocabulary too large for the device's LDS");
-  e = hipFuncSetAttribute(reinterpret_cast<const void *>(fn), hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-  if (e != hipSuccess) return hip_error(e, "hipFuncSetAttribute");
+  KernelInfo ki;
+  int rc0 = kernel_info(fn, sh.W, dyn, di.lds_per_block, &ki);
+  if (rc0 != FUSION_OK) return rc0;
+  hipError_t e = hipSuccess;
   p.s_off = 0;
   p.xcd_map = 0;
   if (p.B == 1 || p.step_mode) {
@@ -1532,10 +1580,7 @@ int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed =
   }
   // beam: every workgroup of a stream must be resident together (cooperative
   // launch); streams beyond what fits at once run in further launches
-  int per_cu = 0;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(fn), sh.W, dyn);
-  if (e != hipSuccess) return hip_error(e, "hipOccupancyMaxActiveBlocksPerMultiprocessor");
-  const long resident = (long)per_cu * di.cus;
+  const long resident = (long)ki.per_cu * di.cus;
   int s_batch = (int)std::min<long>(p.S, resident / p.B);
   // exchange records: 2 buffers x B x k candidates x (3 + n_lm (+1 recombining)) words per stream
   const size_t stream_words = (size_t)2 * p.B * p.k * (3 + p.n_lm + (p.recombine ? 1 : 0));
@@ -1558,13 +1603,15 @@ int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed =
     const int ns = std::min(s_batch, p.S - s0);
     // tag 0 (no frame uses it) everywhere, so that neither uninitialised memory
     // nor an earlier batch's records can pass for the current frame's
-    const int n_ints = (int)(xwords * 2);
-    hipLaunchKernelGGL(zero_ints, dim3(std::min(64, (n_ints + 255) / 256)), dim3(256), 0, stream,
-                       reinterpret_cast<int *>(xbuf), n_ints);
-    e = hipGetLastError();
-    if (e != hipSuccess) {
-      rc = hip_error(e, "exchange reset launch");
-      break;
+    if (!(keep_exchange && s_batch >= p.S)) {
+      const int n_ints = (int)(xwords * 2);
+      hipLaunchKernelGGL(zero_ints, dim3(std::min(64, (n_ints + 255) / 256)), dim3(256), 0, stream,
+                         reinterpret_cast<int *>(xbuf), n_ints);
+      e = hipGetLastError();
+      if (e != hipSuccess) {
+        rc = hip_error(e, "exchange reset launch");
+        break;
+      }
     }
     Params q = p;
     q.s_off = s0;
@@ -1649,7 +1696,8 @@ int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, c
              const float *logits, int32_t T, int32_t S, int32_t B, int32_t V, int32_t k, float beta,
              int32_t blank_id, int32_t blank_mode, int32_t *lm_state, int32_t *boost_state, double *hyp_score,
              int32_t *tokens, int32_t *parents, float *fused, int64_t *traffic, int32_t flags, uint64_t *hist,
-             hipStream_t stream, bool no_alloc = false) {
+             hipStream_t stream, bool no_alloc = false, unsigned long long *xbuf = nullptr, size_t xbuf_words = 0,
+             int32_t t_base = 0) {
   int rc = check_common(lms, alphas, n_lm, trie, logits, V, k, blank_id, blank_mode, beta, T != 0 && S != 0);
   if (rc != FUSION_OK) return rc;
   if (T < 0 || S < 0 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
@@ -1680,6 +1728,8 @@ int run_impl(const NgramTables *const *lms, const float *alphas, int32_t n_lm, c
   p.beta = beta;
   p.recombine = (flags & FUSION_RUN_RECOMBINE) && B > 1;
   p.hist = p.recombine ? reinterpret_cast<unsigned long long *>(hist) : nullptr;
+  p.t_base = t_base;
+  if (xbuf) return launch(p, S * B, stream, xbuf, xbuf_words, t_base > 0);
   if (no_alloc) {
     unsigned long long *xs = nullptr;
     rc = static_scratch(&xs);
@@ -1758,4 +1808,45 @@ extern "C" int fusion_run_lms_noalloc(const NgramTables *const *lms, const float
                                       int64_t *traffic, int32_t flags, uint64_t *hist, hipStream_t stream) {
   return run_impl(lms, alphas, n_lm, trie, logits, T, S, B, V, k, beta, blank_id, blank_mode, lm_state,
                   boost_state, hyp_score, tokens, parents, fused, traffic, flags, hist, stream, true);
+}
+
+extern "C" int fusion_run_projected(const NgramTables *const *lms, const float *alphas, int32_t n_lm,
+                                    const BoostTrie *trie, const uint16_t *A, const uint16_t *W, const float *bias,
+                                    int32_t K, float *logits, int32_t chunk, int32_t T, int32_t S, int32_t B,
+                                    int32_t V, int32_t k,
+                                    float beta, int32_t blank_id, int32_t blank_mode, int32_t *lm_state,
+                                    int32_t *boost_state, double *hyp_score, int32_t *tokens, int32_t *parents,
+                                    int32_t flags, uint64_t *hist, hipStream_t stream) {
+  int rc = check_common(lms, alphas, n_lm, trie, nullptr, V, k, blank_id, blank_mode, beta, false);
+  if (rc != FUSION_OK) return rc;
+  if (T < 0 || S < 0 || B < 1 || B > FUSION_MAX_BEAM) return set_error(FUSION_E_ARG, "T, S or B out of range");
+  if ((int64_t)S * B > (1 << 24)) return set_error(FUSION_E_ARG, "too many hypotheses");
+  if (chunk < 1) return set_error(FUSION_E_ARG, "chunk must be at least 1");
+  if (T == 0 || S == 0) return FUSION_OK;
+  if (!A || !W || !logits) return set_error(FUSION_E_ARG, "NULL joint states, weight or logits workspace");
+  const int64_t H = (int64_t)S * B;
+  const int32_t C = std::min(chunk, T);
+  if ((int64_t)C * H > INT32_MAX) return set_error(FUSION_E_ARG, "chunk * H exceeds the projection's row count");
+  // the beam's exchange records, allocated once for all chunks (every stream at once)
+  unsigned long long *xbuf = nullptr;
+  size_t xwords = 0;
+  if (B > 1) {
+    xwords = (size_t)S * 2 * B * k * (3 + n_lm + ((flags & FUSION_RUN_RECOMBINE) ? 1 : 0));
+    hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&xbuf), xwords * sizeof(unsigned long long), stream);
+    if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
+  }
+  for (int32_t t = 0; t < T && rc == FUSION_OK; t += C) {
+    const int32_t n = std::min(C, T - t);
+    // the chunk's logits of all H hypotheses from their joint hidden states
+    rc = joint_project(A + (size_t)t * H * K, W, bias, (int32_t)(n * H), V, K, logits, stream);
+    if (rc != FUSION_OK) break;
+    rc = run_impl(lms, alphas, n_lm, trie, logits, n, S, B, V, k, beta, blank_id, blank_mode, lm_state, boost_state,
+                  hyp_score, tokens + (size_t)t * H, parents ? parents + (size_t)t * H : nullptr, nullptr, nullptr,
+                  flags, hist, stream, false, xbuf, xwords, t);
+  }
+  if (xbuf) {
+    const hipError_t e = hipFreeAsync(xbuf, stream);
+    if (rc == FUSION_OK && e != hipSuccess) rc = hip_error(e, "hipFreeAsync");
+  }
+  return rc;
 }

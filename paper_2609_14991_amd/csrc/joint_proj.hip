@@ -200,6 +200,12 @@ __global__ void __launch_bounds__(64 * kWM * kWN) joint_proj_kernel(const uint16
   }
 }
 
+// a launch shape of joint_proj_kernel
+template <int WM_, int WN_, int BK_, int TM_, int TN_>
+struct ProjCfg {
+  static constexpr int WM = WM_, WN = WN_, BK = BK_, TM = TM_, TN = TN_;
+};
+
 }  // namespace
 }  // namespace fusion
 
@@ -214,16 +220,21 @@ extern "C" int joint_project(const uint16_t *A, const uint16_t *W, const float *
   if (M == 0) return FUSION_OK;
   if (!A || !W || !out) return set_error(FUSION_E_ARG, "NULL operand");
   if (((uintptr_t)A | (uintptr_t)W) % 16 != 0) return set_error(FUSION_E_ARG, "A and W must be 16-byte aligned");
-  // 256 x 256 tiles, 8 waves of 128 x 64, K stages of 32
-  constexpr int WM = 2, WN = 4, BK = 32, TM = 8, TN = 4;
-  constexpr int BM = 16 * TM * WM, BN = 16 * TN * WN;
-  const int nct = (N + BN - 1) / BN, nrt = (M + BM - 1) / BM;
-  if ((int64_t)nct * nrt > 0x7FFFFFFFll) return set_error(FUSION_E_UNSUPPORTED, "too many tiles");
   // whole 16-byte row segments when every row starts 16-byte aligned
   const int vec_out = (N % 4 == 0 && (uintptr_t)out % 16 == 0) ? 1 : 0;
-  const int xcd_map = (nrt % 4 == 0 && nct % 2 == 0) ? 1 : 0;
-  hipLaunchKernelGGL((joint_proj_kernel<WM, WN, BK, TM, TN>), dim3(nct * nrt), dim3(64 * WM * WN), 0, stream, A, W,
-                     bias, M, N, K, nct, xcd_map, vec_out, out);
-  const hipError_t e = hipGetLastError();
-  return e == hipSuccess ? FUSION_OK : hip_error(e, "joint projection launch");
+  auto go = [&](auto cfg) -> int {
+    using C = decltype(cfg);
+    constexpr int BM = 16 * C::TM * C::WM, BN = 16 * C::TN * C::WN;
+    const int nct = (N + BN - 1) / BN, nrt = (M + BM - 1) / BM;
+    if ((int64_t)nct * nrt > 0x7FFFFFFFll) return set_error(FUSION_E_UNSUPPORTED, "too many tiles");
+    const int xcd_map = (nrt % 4 == 0 && nct % 2 == 0) ? 1 : 0;
+    hipLaunchKernelGGL((joint_proj_kernel<C::WM, C::WN, C::BK, C::TM, C::TN>), dim3(nct * nrt), dim3(64 * C::WM * C::WN),
+                       0, stream, A, W, bias, M, N, K, nct, xcd_map, vec_out, out);
+    const hipError_t e = hipGetLastError();
+    return e == hipSuccess ? FUSION_OK : hip_error(e, "joint projection launch");
+  };
+  // large batches (all frames at once): 256 x 256 tiles, 8 waves of 128 x 64;
+  // one frame's hypotheses (M of a few hundred): 64 x 64 tiles, 4 waves of 16 x
+  // 64, so that the launch still spreads over the CUs.  K stages of 32.
+  return M <= 4096 ? go(ProjCfg<4, 1, 32, 1, 4>{}) : go(ProjCfg<2, 4, 32, 8, 4>{});
 }

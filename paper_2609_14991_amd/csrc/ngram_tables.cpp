@@ -15,23 +15,33 @@ namespace {
 struct DeviceUpload {
   NgramTables *t;
   hipStream_t stream;
+  // pad: zeroed bytes after the data (the kernels read state records with
+  // fixed-size scalar loads that may run past the last record)
   template <class T, class D>
-  int put(const std::vector<T> &h, const D **dst) {
+  int put(const std::vector<T> &h, const D **dst, size_t pad = 0) {
     static_assert(sizeof(T) == sizeof(D), "host and device element sizes differ");
     void *p = nullptr;
-    size_t bytes = std::max<size_t>(h.size() * sizeof(T), 16);
+    const size_t data = h.size() * sizeof(T);
+    size_t bytes = std::max<size_t>(data + pad, 16);
     hipError_t e = hipMalloc(&p, bytes);
     if (e != hipSuccess) return e == hipErrorOutOfMemory ? fusion::set_error(FUSION_E_NOMEM, "device allocation failed") : fusion::hip_error(e, "hipMalloc");
     t->allocs[t->n_allocs++] = p;
     t->device_bytes += (int64_t)bytes;
-    if (!h.empty()) {
-      e = hipMemcpyAsync(p, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice, stream);
+    if (data) {
+      e = hipMemcpyAsync(p, h.data(), data, hipMemcpyHostToDevice, stream);
       if (e != hipSuccess) return fusion::hip_error(e, "hipMemcpyAsync");
+    }
+    if (pad) {
+      e = hipMemsetAsync(static_cast<char *>(p) + data, 0, bytes - data, stream);
+      if (e != hipSuccess) return fusion::hip_error(e, "hipMemsetAsync");
     }
     *dst = (const D *)p;
     return FUSION_OK;
   }
 };
+
+// the kernels read kRecW = 16 words from the start of any record
+constexpr size_t kRecordPad = 64;
 
 }  // namespace
 
@@ -64,14 +74,14 @@ extern "C" int ngram_load(int32_t order, int32_t vocab, int32_t blank_id, const 
   std::memcpy(t->n, h.n, sizeof t->n);
   DeviceUpload up{t, stream};
   if (rc == FUSION_OK) rc = up.put(h.dense, &d.dense);
-  if (rc == FUSION_OK) rc = up.put(h.rec_dense, &d.rec_dense);
+  if (rc == FUSION_OK) rc = up.put(h.rec_dense, &d.rec_dense, kRecordPad);
   if (rc == FUSION_OK) rc = up.put(h.cnt1, &d.cnt1);
   if (rc == FUSION_OK) rc = up.put(h.eos1, &d.eos1);
-  if (rc == FUSION_OK) rc = up.put(h.rec, &d.rec);
+  if (rc == FUSION_OK) rc = up.put(h.rec, &d.rec, kRecordPad);
   if (rc == FUSION_OK) rc = up.put(h.arcs, &d.arcs);
   if (rc == FUSION_OK) rc = up.put(h.top_next, &d.top_next);
   if (rc == FUSION_OK) rc = up.put(h.ctx_lm, &d.ctx_lm);
-  if (rc == FUSION_OK) rc = up.put(h.ctx_rec, &d.ctx_rec);
+  if (rc == FUSION_OK) rc = up.put(h.ctx_rec, &d.ctx_rec, kRecordPad);
   if (rc == FUSION_OK) {
     hipError_t e = hipStreamSynchronize(stream);
     if (e != hipSuccess) rc = fusion::hip_error(e, "hipStreamSynchronize");
