@@ -186,6 +186,13 @@ __device__ __forceinline__ int ord_key(float x) {
   return b ^ ((b >> 31) & 0x7FFFFFFF);
 }
 __device__ __forceinline__ float key_of(int i) { return __int_as_float(i ^ ((i >> 31) & 0x7FFFFFFF)); }
+// (order-preserving key image, token id) as one unsigned 64-bit value, larger
+// for a higher key and, at equal keys, for a lower id
+__device__ __forceinline__ unsigned long long sel_order(int key, int y) {
+  return ((unsigned long long)((uint32_t)key ^ 0x80000000u) << 32) | (unsigned long long)(~(uint32_t)y);
+}
+// the key of a composite's upper half
+__device__ __forceinline__ int sel_key(int hi) { return (int)((uint32_t)hi ^ 0x80000000u); }
 // uniform maximum of an int over the wave (identity INT_MIN)
 template <int CTRL, int ROWS>
 __device__ __forceinline__ int dpp_i(int v) {
@@ -285,11 +292,16 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   int *sTN = sDT + kAux;  // [NL][kAux]
   __shared__ float s_pm[kMaxWaves], s_ps[kMaxWaves];
   __shared__ int s_paid[kMaxWaves];
+  __shared__ float s_lse;  // the current frame's log-sum-exp of the logits row
+  __shared__ int s_am;     // and the lowest id holding its maximum
+  __shared__ int s_nstat;  // waves done with the next frame's strip statistics
   __shared__ int w_key[kMaxWaves][KM];  // order-preserving images of the keys (ord_key)
   __shared__ int w_y[kMaxWaves][KM];
-  __shared__ int s_wmax[kMaxWaves];  // each wave's best key (KM > 1)
-  __shared__ __align__(16) int2 s_sel[16];  // the hypothesis' listed entries (key, id), compacted
-  __shared__ int2 s_win[KM];                // its top K by rank
+  // each wave's best key with its wave index, and the hypothesis' listed entries
+  // (compacted) and top K, all as sel_order composites (KM > 1)
+  __shared__ __align__(16) unsigned long long s_wmax[kMaxWaves];
+  __shared__ __align__(16) unsigned long long s_sel[16];
+  __shared__ unsigned long long s_win[KM];
   __shared__ HypState<NL> hs;
   // beam rendezvous staging (wave 0): candidate records (the second LM's source
   // and c_1 in s_xb), parent flags, totals
@@ -372,7 +384,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       ok_lm = ok_lm && ok_i;
       hs.lmsrc[i] = sig;
       hs.c1p[i] = -1;
-      hs.c1[i] = (ok_i && sig < V + 2) ? sig : -1;
+      // c_1, the last token of the state: the state itself below V + 2, else
+      // from its record (so that every frame knows c_1 before its record arrives)
+      hs.c1[i] = !ok_i ? -1 : sig < V + 2 ? sig : (lms[i].rec[(int64_t)(sig - V - 2) * lms[i].rec_stride] & 0xFFFF);
       hs.cur_lm[i] = sig;
     }
     const bool ok_q = !p.has_trie || (q >= 0 && q < tr.n_nodes);
@@ -483,6 +497,21 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       s_paid[sw] = aid;
     }
   };
+  // the strip statistics of all NW waves combined into s_lse / s_am (one wave)
+  auto combine_stats = [&]() {
+    const bool wl = lane < NW;
+    const float pm = wl ? s_pm[lane] : -INFINITY;
+    const float M = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_max(pm)), 0));
+    const float term = (wl && pm > -INFINITY) ? s_ps[lane] * exp_fast(pm - M) : 0.0f;
+    const float lse = M + logf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_sum(term)), 0)));
+    float ak = pm;
+    int ay = wl ? s_paid[lane] : INT_MAX;
+    row_best(ak, ay);
+    if (lane == 0) {
+      s_lse = lse;
+      s_am = ay;
+    }
+  };
   // a V-wide fp32 row straight from HBM into an LDS row (this wave's strips)
   auto load_row = [&](const float *drow, float *row, int V) {
 #pragma unroll
@@ -501,6 +530,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     }
   };
   row_stats(xraw, wave, p.V);
+  if (g == 0) s_nstat = 0;
+  __syncthreads();
+  if (wave == NW - 1) combine_stats();
+  __syncthreads();
 
   bool aborted = false;  // after one failed rendezvous this workgroup stops waiting
   for (int t = 0; t < p.T; ++t) {
@@ -563,15 +596,16 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const int node[4] = {nq[0], nq[1], nq[2], nq[3]};
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
-      // the initial state of a run may need its record to learn c_1
-      if (ok && c1[i] < 0) c1[i] = rp[i] ? (rec[i][0] & 0xFFFF) : lmsrc[i];
       // level-1 dense row straight into the LM's LDS row.  Issued
       // unconditionally (row 0 stands in when the hypothesis has no keys to
       // compute this frame), so that only the records are waited for before the
       // second hop
       load_row(lms[i].dense + (int64_t)(ok ? c1[i] : 0) * V, lmval + i * Vp, V);
     }
-    if (NW == 1 && t > 0) row_stats(xraw, 0, V);  // a single wave has no idle helper
+    if (NW == 1 && t > 0) {  // a single wave has no idle helper
+      row_stats(xraw, 0, V);
+      combine_stats();
+    }
     // ---- decode the records ---------------------------------------------------------
     const float phiq = as_float(node[0]);
     const int dbeg = node[1];
@@ -737,24 +771,11 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     }
     __builtin_amdgcn_s_waitcnt(0);  // the dense rows have landed in LDS
     __syncthreads();
-    // ---- combine the row statistics (lanes 0..NW-1 hold one wave each) --------------
+    // ---- the row statistics of this frame ---------------------------------------------
     // the log-sum-exp is needed by wave 0 (selected scores, beam totals) and, for
     // fused rows, by every wave; the acoustic argmax (mode A) by every wave
-    float lse = 0.0f;
-    int am = INT_MAX;
-    if (wave == 0 || p.fused != nullptr || p.mode == FUSION_BLANK_AM) {
-      const bool wl = lane < NW;
-      const float pm = wl ? s_pm[lane] : -INFINITY;
-      const float M = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_max(pm)), 0));
-      const float term = (wl && pm > -INFINITY) ? s_ps[lane] * exp_fast(pm - M) : 0.0f;
-      lse = M + logf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(row_sum(term)), 0)));
-      if (p.mode == FUSION_BLANK_AM) {
-        float ak = pm;
-        int ay = wl ? s_paid[lane] : INT_MAX;
-        row_best(ak, ay);
-        am = __builtin_amdgcn_readlane(ay, 0);
-      }
-    }
+    const float lse = __int_as_float(uni(__float_as_int(s_lse)));
+    const int am = uni(s_am);
     // ---- keys and the fused row ------------------------------------------------------
     const bool blank_only = inv || (p.mode == FUSION_BLANK_AM && am == blank);
     const bool want_keys = ok && (!blank_only || p.fused);
@@ -902,19 +923,19 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
 #pragma unroll
         for (int c = 0; c < NC; ++c) lb = max(lb, max(max(sk[c][0], sk[c][1]), max(sk[c][2], sk[c][3])));
         const int mw = wave_max_i(lb);
-        if (lane == 0) s_wmax[wave] = mw;
+        if (lane == 0) s_wmax[wave] = sel_order(mw, wave);
         lds_barrier();
         int tau = INT_MIN;
         if (NW >= K) {
-          // lanes 0..NW-1 (one row) hold the maxima; K-1 rounds each drop one
-          // instance of the row maximum, then the maximum left is the K-th largest
-          int v = lane < NW ? s_wmax[lane] : INT_MIN;
-          for (int r = 0; r + 1 < K; ++r) {
-            const int m = row_max_i(v);
-            const unsigned long long own = __ballot(v == m) & 0xFFFFull;
-            v = lane == __ffsll((long long)own) - 1 ? INT_MIN : v;
-          }
-          tau = __builtin_amdgcn_readlane(row_max_i(v), 0);
+          // the K-th largest of the NW maxima (counted with multiplicity): lane
+          // l < NW ranks maximum l among all of them (ties by wave index) and the
+          // lane of rank K-1 holds it
+          const unsigned long long mine = s_wmax[lane < NW ? lane : 0];
+          int r = 0;
+#pragma unroll
+          for (int w2 = 0; w2 < NW; ++w2) r += (int)(s_wmax[w2] > mine);
+          const unsigned long long at = __ballot(lane < NW && r == K - 1);
+          tau = sel_key(__builtin_amdgcn_readlane((int)(mine >> 32), __ffsll((long long)at) - 1));
         }
         // survivors: keys >= tau, never a non-candidate (INT_MIN; every real key,
         // -inf included, maps above it)
@@ -1012,10 +1033,17 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       s_steps += 1ull;
     }
     lds_barrier();
-    // the next frame's row statistics
+    // the next frame's row statistics, by the waves other than wave 0; the last of
+    // them to finish combines them (ahead of the frame's end, off wave 0's path)
     if (NW > 1 && wave != 0 && t + 1 < p.T) {
       row_stats(xraw, wave, V);
       if (wave == 1) row_stats(xraw0, 0, V);
+      int done = 0;
+      if (lane == 0) done = __hip_atomic_fetch_add(&s_nstat, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (uni(done) == NW - 2) {
+        combine_stats();
+        if (lane == 0) s_nstat = 0;
+      }
     }
     // ---- the hypothesis' top-k (wave 0): the K-entry lists of the NW waves spread
     // over the lanes (entry j of wave w is element e = j*NW + w, lane e % 64, slot
@@ -1042,30 +1070,30 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         const int n = __popcll(vb);
         if (n <= 16) {
           const int pos = __builtin_amdgcn_mbcnt_hi((uint32_t)(vb >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)vb, 0u));
-          if (valid) s_sel[pos] = make_int2(ek[0], ey[0]);
-          if (lane >= n && lane < 16) s_sel[lane] = make_int2(INT_MIN, INT_MAX);
+          // an entry is ahead of another exactly when its composite is larger;
+          // padding (0) is never ahead of a listed entry (every key is above INT_MIN)
+          if (valid) s_sel[pos] = sel_order(ek[0], ey[0]);
+          if (lane >= n && lane < 16) s_sel[lane] = 0ull;
           // one wave: its LDS operations complete in order
           asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-          int kv[16], yv[16];
+          unsigned long long cv[16];
 #pragma unroll
           for (int q = 0; q < 16; q += 2) {
-            const int4 d = *reinterpret_cast<const int4 *>(&s_sel[q]);
-            kv[q] = d.x;
-            yv[q] = d.y;
-            kv[q + 1] = d.z;
-            yv[q + 1] = d.w;
+            const ulonglong2 d = *reinterpret_cast<const ulonglong2 *>(&s_sel[q]);
+            cv[q] = d.x;
+            cv[q + 1] = d.y;
           }
-          const int2 me = s_sel[lane & 15];
+          const unsigned long long me = s_sel[lane & 15];
           int r = 0;
 #pragma unroll
-          for (int q = 0; q < 16; ++q) r += (int)((kv[q] > me.x) | ((kv[q] == me.x) & (yv[q] < me.y)));
+          for (int q = 0; q < 16; ++q) r += (int)(cv[q] > me);
           if (lane < n && r < K) s_win[r] = me;
           asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
           const int nk = min(n, K);
-          const int2 wv = s_win[lane < nk ? lane : 0];
+          const unsigned long long wv = s_win[lane < nk ? lane : 0];
           if (lane < nk) {
-            ck = wv.x;
-            cy = wv.y;
+            ck = sel_key((int)(wv >> 32));
+            cy = (int)~(uint32_t)wv;
           }
           picked = true;
         }
