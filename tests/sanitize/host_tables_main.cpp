@@ -4,10 +4,12 @@
 // write_case in the test), builds both host layouts and prints their sizes
 // and a checksum of every array, or the error code the builders return.
 // With a second argument it also writes the state records, the context rows
-// and the level-1 next-state records there.
+// and the level-1 next-state records there ("-": not written); with a third,
+// the phrase tree's nodes, transition lists, root row and root entry values.
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
+#include <string>
 #include <vector>
 
 #include "tables_host.h"
@@ -31,6 +33,12 @@ T read_one() {
   return read_vec<T>(1)[0];
 }
 
+// a vector's bytes to f (nothing for an empty one: fwrite takes no null pointer)
+template <class T>
+void put(FILE *f, const std::vector<T> &v) {
+  if (!v.empty()) fwrite(v.data(), sizeof(T), v.size(), f);
+}
+
 template <class T>
 uint64_t sum_bytes(const std::vector<T> &v) {
   uint64_t h = 1469598103934665603ull;  // FNV-1a over the bytes
@@ -42,7 +50,7 @@ uint64_t sum_bytes(const std::vector<T> &v) {
 }  // namespace
 
 int main(int argc, char **argv) {
-  if (argc != 2 && argc != 3) return 2;
+  if (argc < 2 || argc > 4) return 2;
   g_in = fopen(argv[1], "rb");
   if (!g_in) return 2;
   const int32_t N = read_one<int32_t>(), V = read_one<int32_t>(), blank = read_one<int32_t>();
@@ -82,14 +90,14 @@ int main(int argc, char **argv) {
            (unsigned long long)sum_bytes(lm.eos1), (unsigned long long)sum_bytes(lm.rec),
            (unsigned long long)sum_bytes(lm.arcs), (unsigned long long)sum_bytes(lm.top_next));
     printf("lm_ctx n_ctx=%lld\n", (long long)lm.n_ctx);
-    if (argc == 3) {  // the records and context rows, for the test to check against the oracle
+    if (argc >= 3 && std::string(argv[2]) != "-") {  // the records and context rows, for the test to check against the oracle
       FILE *f = fopen(argv[2], "wb");
       const int64_t hdr[4] = {lm.rec_stride, lm.n_ctx, (int64_t)lm.rec.size(), (int64_t)lm.rec_dense.size()};
       fwrite(hdr, sizeof hdr, 1, f);
-      fwrite(lm.rec.data(), 4, lm.rec.size(), f);
-      fwrite(lm.ctx_lm.data(), 4, lm.ctx_lm.size(), f);
-      fwrite(lm.ctx_rec.data(), 4, lm.ctx_rec.size(), f);
-      fwrite(lm.rec_dense.data(), 4, lm.rec_dense.size(), f);
+      put(f, lm.rec);
+      put(f, lm.ctx_lm);
+      put(f, lm.ctx_rec);
+      put(f, lm.rec_dense);
       fclose(f);
     }
   }
@@ -103,6 +111,17 @@ int main(int argc, char **argv) {
     printf("trie_sums %llx %llx %llx %llx\n", (unsigned long long)sum_bytes(tr.node),
            (unsigned long long)sum_bytes(tr.delta), (unsigned long long)sum_bytes(tr.root_node),
            (unsigned long long)sum_bytes(tr.root_E));
+    if (argc == 4) {  // the phrase tree, for the test to check against brute force
+      FILE *f = fopen(argv[3], "wb");
+      const int64_t hdr[4] = {tr.n_nodes, (int64_t)tr.delta.size(), (int64_t)tr.root_node.size(),
+                              (int64_t)tr.root_E.size()};
+      fwrite(hdr, sizeof hdr, 1, f);
+      put(f, tr.node);
+      put(f, tr.delta);
+      put(f, tr.root_node);
+      put(f, tr.root_E);
+      fclose(f);
+    }
   }
   return 0;
 }

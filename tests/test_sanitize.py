@@ -8,6 +8,7 @@ builders run on the C1 and C2/C3 models and phrase lists and on malformed
 input; the oracle runs its CPU pins in a child interpreter with the sanitized
 library preloaded.  Any report from either sanitizer fails the test."""
 
+import bisect
 import os
 import subprocess
 import sys
@@ -157,3 +158,140 @@ def test_context_rows_equal_the_backoff_recursion(driver, tmp_path, seed, N, X):
                 want = (L << 28) | index[t[-L:]]
                 break
         assert rec[sid - V - 2, cw] == want, (t, rec[sid - V - 2, cw], want)
+
+
+def _dump_tables(driver, tmp_path, lm, ph, name):
+    """Both host layouts of a model and a phrase list, from the sanitized builders."""
+    path, lmd, trd = (str(tmp_path / f"{name}.{s}") for s in ("bin", "lm", "tr"))
+    write_case(path, lm, ph)
+    r = subprocess.run([driver, path, lmd, trd], capture_output=True, text=True, env=ENV, timeout=600)
+    assert r.returncode == 0 and "runtime error" not in r.stderr and "ERROR" not in r.stderr, r.stderr[-2000:]
+    with open(lmd, "rb") as f:
+        RS, _, n_rec, _ = (int(v) for v in np.frombuffer(f.read(32), np.int64))
+        rec = np.frombuffer(f.read(4 * n_rec), np.int32).reshape(-1, RS)
+    with open(trd, "rb") as f:
+        n_nodes, n_delta, n_root, n_re = (int(v) for v in np.frombuffer(f.read(32), np.int64))
+        node = np.frombuffer(f.read(16 * n_nodes), np.int32).reshape(-1, 4)
+        delta = np.frombuffer(f.read(16 * n_delta), np.int32).reshape(-1, 4)
+        root_node = np.frombuffer(f.read(16 * n_root), np.int32).reshape(-1, 4)
+        root_E = np.frombuffer(f.read(4 * n_re), np.float32)
+    return rec, (node, delta, root_node, root_E)
+
+
+@pytest.mark.parametrize("seed,N", [(0, 3), (1, 4), (2, 5), (3, 6)])
+def test_state_records_follow_the_oracle_numbering(driver, tmp_path, seed, N):
+    """Every state record of the builders against the definitions: state sid
+    is the oracle's context t = state_tuple(sid) (ids by order, then
+    lexicographic rank, numbered by the oracle on its own); the record holds
+    c_1 = t[-1], the order m = |t|, the id, and for each level L = 2..m the
+    backoff of t's last L tokens read straight from the input tuples and
+    their number of one-token extensions counted over the raw n-gram rows; the
+    first-arc words of contexts with arcs advance with the number of arcs of
+    the lexicographically smaller contexts."""
+    import oracle
+
+    rng = np.random.default_rng(970 + seed)
+    V = 19
+    lm = tiny_random_lm(rng, V, N, n_sent=300, cutoffs=tuple([1] * N))
+    ph = tiny_random_phrases(rng, V, n=4, max_len=3)
+    rec, _ = _dump_tables(driver, tmp_path, lm, ph, "rec")
+    olm = oracle.OracleLM(lm)
+    assert olm.n_states == V + 2 + rec.shape[0]
+    bo, rows_by_len = {}, {}
+    for k in range(1, N):
+        toks = [tuple(int(v) for v in t) for t in lm.tokens[k - 1]]
+        for t, b in zip(toks, lm.backoff[k - 1]):
+            bo[t] = np.float32(b)
+    for k in range(2, N + 1):
+        rows_by_len[k - 1] = sorted(tuple(int(v) for v in t[:k - 1]) for t in lm.tokens[k - 1])
+    offset_of_level = {}
+    for sid in range(V + 2, V + 2 + rec.shape[0]):
+        r, t = rec[sid - V - 2], olm.state_tuple(sid)
+        m = len(t)
+        assert 2 <= m <= N - 1
+        assert r[0] == (t[-1] | (m << 16)) and r[1] == sid, (sid, t, r[:2])
+        for L in range(2, m + 1):
+            c = t[-L:]
+            pre = rows_by_len[L]
+            lo = bisect.bisect_left(pre, c)
+            cnt = bisect.bisect_right(pre, c) - lo
+            assert np.float32(r[2 + 3 * (L - 2)].view(np.float32)) == bo.get(c, np.float32(0.0)), (t, L)
+            assert r[4 + 3 * (L - 2)] == cnt, (t, L, r[4 + 3 * (L - 2)], cnt)
+            # first arc = a per-level base + the number of arcs of smaller
+            # contexts (a context with no arcs has no first arc to check)
+            if cnt:
+                base = int(r[3 + 3 * (L - 2)]) - lo
+                assert offset_of_level.setdefault(L, base) == base, (t, L)
+
+
+def _prefix_numbering(phrases):
+    """Phrase-tree node ids from the definition: every phrase prefix, the
+    root first, ranked by (length, tokens)."""
+    pre = {()}
+    for p in phrases:
+        for L in range(1, len(p) + 1):
+            pre.add(tuple(p[:L]))
+    nodes = sorted(pre, key=lambda t: (len(t), t))
+    return nodes, {t: i for i, t in enumerate(nodes)}
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_phrase_transitions_are_the_longest_prefix_suffix(driver, tmp_path, seed):
+    """The phrase tree with its failure links compiled out, against brute
+    force: for every node q and token y, the transition (q's own list if y is
+    in it, else the root's row) is the longest suffix of q y that is a phrase
+    prefix; q's list holds exactly the tokens whose transition differs from
+    the root's, sorted; every entry value is E = fl32(Phi + out) of R9 with
+    Phi and out computed from the phrase list (out adding the completion
+    bonuses of the phrases that end the prefix, shortest first).  The oracle's
+    own node numbering is checked against the same definition."""
+    import oracle
+
+    rng = np.random.default_rng(990 + seed)
+    V = 11
+    lm = tiny_random_lm(rng, V, 3, n_sent=60)
+    ph = tiny_random_phrases(rng, V, n=12, max_len=5, alphabet=4)
+    plist = [tuple(int(v) for v in p) for p in ph.as_lists()]
+    _, (node, delta, root_node, root_E) = _dump_tables(driver, tmp_path, lm, ph, "trie")
+    nodes, nid = _prefix_numbering(plist)
+    assert node.shape[0] == len(nodes)
+    otr = oracle.OracleTrie(V, 0, ph)
+    for q, t in enumerate(nodes):
+        assert tuple(otr.node_tuple(q)) == t
+    ts = np.float32(ph.token_score)
+    bonus = {}
+    for i, p in enumerate(plist):
+        if p not in bonus:  # a repeated phrase keeps its first bonus
+            bonus[p] = np.float32(ph.completion[i]) if ph.completion is not None else np.float32(ts * np.float32(len(p)))
+
+    def E(t):
+        phi = np.float32(0.0) if t in bonus else np.float32(np.float32(len(t)) * ts)
+        out = np.float32(0.0)
+        for L in range(1, len(t) + 1):
+            if t[-L:] in bonus:
+                out = np.float32(out + bonus[t[-L:]])
+        return np.float32(phi + out)
+
+    def target(t, y):
+        s = t + (y,)
+        for L in range(len(s), 0, -1):
+            if s[-L:] in nid:
+                return nid[s[-L:]]
+        return 0
+
+    for y in range(1, V):
+        g = target((), y)
+        assert root_node[y, 3] == g and root_E[y] == E(nodes[g]), y
+    for q, t in enumerate(nodes):
+        phi_bits, beg, cnt, qq = (int(v) for v in node[q])
+        assert qq == q
+        assert np.int32(phi_bits).view(np.float32) == (np.float32(0.0) if t in bonus else np.float32(np.float32(len(t)) * ts))
+        own = {int(d[0]): (int(d[1]), np.int32(d[2]).view(np.float32)) for d in delta[beg:beg + cnt]}
+        assert [int(d[0]) for d in delta[beg:beg + cnt]] == sorted(own)
+        for y in range(1, V):
+            want = target(t, y)
+            if y in own:
+                assert own[y][0] == want and own[y][0] != root_node[y, 3], (t, y)
+                assert own[y][1] == E(nodes[want]), (t, y)
+            else:
+                assert root_node[y, 3] == want, (t, y, want)
