@@ -361,7 +361,7 @@ def producer_leg(F, torch, dev, stream, w, lm, trie, a_d, w_d, b_d, o_d, K, n_la
     res["decisions_equal"] = bool(same)
     res["note"] = ("chunk_c: fusion_run_projected with c frames per projection ([c*H, K] x [K, V] into a [c, H, V] "
                    "workspace, then one decode launch of those c frames); batched: one [T*H, K] x [K, V] projection "
-                   "then one fusion_run; each launch of a beam decode is cooperative (a fixed cost per launch)")
+                   "then one fusion_run")
     log("producer loop (C5): " + ", ".join(f"{n} {res[n]['ms']:.3f} ms" for n in runs) + f", decisions equal {same}")
     return res
 

@@ -85,6 +85,7 @@ struct Params {
   int32_t *next_boost;
   unsigned long long *xchg;  // beam exchange [S][2][B][k] candidate records of four tagged words
   unsigned long long *hist;  // recombination: [H] in/out history hashes (0: derive from the initial states) or NULL
+  unsigned *tickets;         // beam: arrival counters, one per blockIdx class (8 with xcd_map, else 1)
   // t_base: the number of frames decoded by earlier calls of a frame loop that
   // keeps the exchange between calls (its records are tagged by global frame)
   int32_t T, S, B, V, k, blank, mode, has_trie, step_mode, s_off, xcd_map, n_lm, recombine, t_base;
@@ -315,6 +316,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
   __shared__ long long s_sbase[NL][kMaxLevels];  // state id of arc index i of level L < N-1: s_sbase[L] + i
   __shared__ int s_lbeg[NL][kMaxLevels];  // first arc of each level of the current state
   __shared__ int s_cfg[2];  // V, blank: re-read each frame so per-token masks stay inside the loop
+  __shared__ int s_ticket;  // beam: this workgroup's arrival ticket
   __shared__ unsigned long long s_bytes, s_steps;
 
   const LMDevice *lms = p.lm;
@@ -345,17 +347,39 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     RSl[i] = lms[i].rec_stride;
   }
   // workgroup -> (stream, hypothesis); with xcd_map the B workgroups of a stream
-  // share blockIdx mod 8, i.e. one XCD and its L2, for the per-frame exchange
+  // share blockIdx mod 8, i.e. one XCD and its L2, for the per-frame exchange.
+  // A beam takes its index r within that class from an arrival counter: the
+  // workgroups that have started always hold the first tickets of each class,
+  // so every stream but the last one started in a class is complete and runs
+  // to its end, freeing room for the rest.  The beam therefore needs no
+  // co-residency guarantee (no cooperative launch), only room for the
+  // incomplete streams beside one complete one (checked at launch)
   int sl, b;
   {
     const int x = blockIdx.x;
+    int r = p.xcd_map ? x >> 3 : x;
+    if constexpr (BEAM) {
+      const int n_cls = p.xcd_map ? (int)(gridDim.x >> 3) : (int)gridDim.x;
+      if (g == 0) {
+        unsigned *ctr = p.tickets + (p.xcd_map ? (x & 7) : 0);
+        const int tk = (int)atomicAdd(ctr, 1u);
+        // the class's last ticket leaves the counter at 0 for the next launch
+        if (tk == n_cls - 1) atomicExch(ctr, 0u);
+        s_ticket = tk;
+      }
+      __syncthreads();
+      r = s_ticket;
+      if (r >= n_cls) {  // counters not reset since an earlier launch: no slot for this workgroup
+        if (g == 0) atomicOr(&g_status, FUSION_STATUS_SYNC_TIMEOUT);
+        return;
+      }
+    }
     if (p.xcd_map) {
-      const int r = x >> 3;
       sl = (x & 7) + 8 * (r / B);
       b = r % B;
     } else {
-      sl = x / B;
-      b = x % B;
+      sl = r / B;
+      b = r % B;
     }
   }
   const int s = sl + p.s_off;
@@ -1606,31 +1630,38 @@ int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed =
     e = hipGetLastError();
     return e == hipSuccess ? FUSION_OK : hip_error(e, "fusion kernel launch");
   }
-  // beam: every workgroup of a stream must be resident together (cooperative
-  // launch); streams beyond what fits at once run in further launches
+  // beam: a stream's workgroups meet every frame.  They take their slots from
+  // arrival counters (see the kernel), so one launch may hold more streams
+  // than fit on the device at once, provided the incomplete streams (one per
+  // blockIdx class, at most 8 x (B - 1) workgroups) cannot fill it
   const long resident = (long)ki.per_cu * di.cus;
-  int s_batch = (int)std::min<long>(p.S, resident / p.B);
-  // exchange records: 2 buffers x B x k candidates x (3 + n_lm (+1 recombining)) words per stream
+  if (resident <= 8L * (p.B - 1)) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device");
+  // exchange records: 2 buffers x B x k candidates x (3 + n_lm (+1 recombining)) words per
+  // stream, then the 8 arrival counters (4 words)
   const size_t stream_words = (size_t)2 * p.B * p.k * (3 + p.n_lm + (p.recombine ? 1 : 0));
+  constexpr size_t kTicketWords = 4;
+  int s_batch = p.S;
   if (fixed) {
-    if (stream_words > fixed_words)
+    if (stream_words + kTicketWords > fixed_words)
       return set_error(FUSION_E_UNSUPPORTED, "one stream's beam exchange exceeds the static scratch");
-    s_batch = (int)std::min<size_t>((size_t)s_batch, fixed_words / stream_words);
+    s_batch = (int)std::min<size_t>((size_t)s_batch, (fixed_words - kTicketWords) / stream_words);
   }
   if (s_batch >= 8) s_batch -= s_batch % 8;
-  if (s_batch < 1) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device at once");
-  const size_t xwords = (size_t)s_batch * stream_words;
+  const size_t xwords = (size_t)s_batch * stream_words + kTicketWords;
   void *xbuf = fixed;
   if (!fixed) {
     e = hipMallocAsync(&xbuf, xwords * sizeof(unsigned long long), stream);
     if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
   }
   p.xchg = reinterpret_cast<unsigned long long *>(xbuf);
+  p.tickets = reinterpret_cast<unsigned *>(p.xchg + (size_t)s_batch * stream_words);
   int rc = FUSION_OK;
   for (int s0 = 0; s0 < p.S && rc == FUSION_OK; s0 += s_batch) {
     const int ns = std::min(s_batch, p.S - s0);
-    // tag 0 (no frame uses it) everywhere, so that neither uninitialised memory
-    // nor an earlier batch's records can pass for the current frame's
+    // tag 0 (no frame uses it) everywhere and the counters at 0, so that neither
+    // uninitialised memory nor an earlier batch's records can pass for the
+    // current frame's (a frame loop that keeps the exchange relies on its
+    // global frame numbers and on the counters resetting themselves)
     if (!(keep_exchange && s_batch >= p.S)) {
       const int n_ints = (int)(xwords * 2);
       hipLaunchKernelGGL(zero_ints, dim3(std::min(64, (n_ints + 255) / 256)), dim3(256), 0, stream,
@@ -1644,9 +1675,9 @@ int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed =
     Params q = p;
     q.s_off = s0;
     q.xcd_map = (ns % 8 == 0) ? 1 : 0;
-    void *args[] = {&q};
-    e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(ns * p.B), dim3(sh.W), args, dyn, stream);
-    if (e != hipSuccess) rc = hip_error(e, "cooperative fusion kernel launch");
+    hipLaunchKernelGGL(fn, dim3(ns * p.B), dim3(sh.W), dyn, stream, q);
+    e = hipGetLastError();
+    if (e != hipSuccess) rc = hip_error(e, "fusion kernel launch");
   }
   if (!fixed) {
     hipError_t e2 = hipFreeAsync(xbuf, stream);
@@ -1859,7 +1890,8 @@ extern "C" int fusion_run_projected(const NgramTables *const *lms, const float *
   unsigned long long *xbuf = nullptr;
   size_t xwords = 0;
   if (B > 1) {
-    xwords = (size_t)S * 2 * B * k * (3 + n_lm + ((flags & FUSION_RUN_RECOMBINE) ? 1 : 0));
+    // every stream's records and the arrival counters (4 words)
+    xwords = (size_t)S * 2 * B * k * (3 + n_lm + ((flags & FUSION_RUN_RECOMBINE) ? 1 : 0)) + 4;
     hipError_t e = hipMallocAsync(reinterpret_cast<void **>(&xbuf), xwords * sizeof(unsigned long long), stream);
     if (e != hipSuccess) return hip_error(e, "hipMallocAsync");
   }
