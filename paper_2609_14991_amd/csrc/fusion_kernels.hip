@@ -57,7 +57,8 @@ constexpr int kMaxWaves = 16;
 constexpr int kMaxLevels = FUSION_MAX_ORDER;  // context levels 1..N-1 <= 5
 constexpr int kAux = 256;                     // LDS side tables: phrase transitions, top-level next states
 constexpr int kRecW = 16;                     // words read per state record: record_stride(FUSION_MAX_ORDER)
-constexpr int kSpinLimit = 1 << 20;           // bounded wait at the beam rendezvous (polls, ~1 s)
+constexpr int kSpinLimit = 1 << 21;           // bounded wait at the beam rendezvous (polls, each waiting
+                                              // for its loads: about a second)
 
 __device__ int g_status;
 __device__ __align__(64) int32_t g_zero_words[16];  // never written: the record and node of "no state"
@@ -1288,7 +1289,6 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
               aborted = true;
               break;
             }
-            __builtin_amdgcn_s_sleep(1);
           }
           if (i < nc) {
             const int y1 = (int)((w[2] >> 32) & 0xFFFF);
@@ -1388,12 +1388,15 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         if (wi >= 0) {
           // the lane holding the slot's candidate installs it
           const int4 a = s_xa[wi];
+          const int xf = s_xf[wi];
+          const double tot = s_tot[wi];
+          int2 xb = make_int2(0, 0);
+          if constexpr (NL > 1) xb = s_xb[wi];
           const int y = a.x;
           int src[NL], c1p[NL];
           src[0] = a.y;
           c1p[0] = a.w;
           if constexpr (NL > 1) {
-            const int2 xb = s_xb[wi];
             src[1] = xb.x;
             c1p[1] = xb.y;
           }
@@ -1405,9 +1408,9 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           }
           hs.qsrc = a.z;
           hs.y = y;
-          hs.fl = 1 | (s_xf[wi] & 2);
+          hs.fl = 1 | (xf & 2);
           if constexpr (RC) hs.hist = s_hh[wi];
-          hs.S = s_tot[wi];
+          hs.S = tot;
           p.tokens[o] = y;
           p.parents[o] = wi / K;
         }
@@ -1631,16 +1634,19 @@ int launch(Params &p, int n_hyp, hipStream_t stream, unsigned long long *fixed =
     return e == hipSuccess ? FUSION_OK : hip_error(e, "fusion kernel launch");
   }
   // beam: a stream's workgroups meet every frame.  They take their slots from
-  // arrival counters (see the kernel), so one launch may hold more streams
-  // than fit on the device at once, provided the incomplete streams (one per
-  // blockIdx class, at most 8 x (B - 1) workgroups) cannot fill it
+  // arrival counters (see the kernel), which keeps a launch free of deadlock
+  // even when other work holds part of the device, provided the incomplete
+  // streams (one per blockIdx class, at most 8 x (B - 1) workgroups) cannot
+  // fill it.  A launch holds no more streams than fit at once, so that no
+  // workgroup waits at a rendezvous for a sibling that has yet to start behind
+  // whole streams (the wait is bounded); further streams run in further launches
   const long resident = (long)ki.per_cu * di.cus;
   if (resident <= 8L * (p.B - 1)) return set_error(FUSION_E_UNSUPPORTED, "a beam does not fit on the device");
   // exchange records: 2 buffers x B x k candidates x (3 + n_lm (+1 recombining)) words per
   // stream, then the 8 arrival counters (4 words)
   const size_t stream_words = (size_t)2 * p.B * p.k * (3 + p.n_lm + (p.recombine ? 1 : 0));
   constexpr size_t kTicketWords = 4;
-  int s_batch = p.S;
+  int s_batch = (int)std::min<long>(p.S, resident / p.B);
   if (fixed) {
     if (stream_words + kTicketWords > fixed_words)
       return set_error(FUSION_E_UNSUPPORTED, "one stream's beam exchange exceeds the static scratch");

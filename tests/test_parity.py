@@ -329,12 +329,11 @@ def test_repeat_runs_are_identical(c2):
         assert torch.equal(a, b)
 
 
-def test_beam_with_more_streams_than_fit():
+def test_beam_in_several_launch_batches():
     """More streams than the device holds at once (160 x 4 workgroups of 1024
-    lanes, 2.5 times the 256 CUs) in one launch: the workgroups that start
-    later take the later arrival tickets, so the streams run in waves and
-    every stream's slots still meet each frame.  Every decision is replayed by
-    the oracle."""
+    lanes, 2.5 times the 256 CUs): the run is split into launch batches of
+    what fits, whose rendezvous buffers and arrival counters are cleared in
+    between.  Every decision is replayed by the oracle."""
     rng = np.random.default_rng(80)
     V, S, B, k, T = 1100, 160, 4, 4, 12
     lm = tiny_random_lm(rng, V, 4, n_sent=3000)
