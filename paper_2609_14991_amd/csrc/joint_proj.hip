@@ -236,5 +236,5 @@ extern "C" int joint_project(const uint16_t *A, const uint16_t *W, const float *
   // large batches (all frames at once): 256 x 256 tiles, 8 waves of 128 x 64;
   // one frame's hypotheses (M of a few hundred): 64 x 64 tiles, 4 waves of 16 x
   // 64, so that the launch still spreads over the CUs.  K stages of 32.
-  return M <= 4096 ? go(ProjCfg<4, 1, 32, 1, 4>{}) : go(ProjCfg<2, 4, 32, 8, 4>{});
+  return M <= 4096 ? go(ProjCfg<4, 1, 64, 1, 4>{}) : go(ProjCfg<2, 4, 32, 8, 4>{});
 }
