@@ -302,9 +302,39 @@ def projection_leg(F, torch, dev, stream, cfg, w=None, lm=None, trie=None):
             "min_hbm_bytes": pbytes, "hbm_gbs_at_min_bytes": pbytes / (pms / 1e3) / 1e9,
         }
         log(f"joint projection {m}x{N}x{K}: {pms * 1e3:.1f} us, {flops / (pms / 1e3) / 1e12:.1f} TFLOP/s")
+        out[name]["vendor_gemm"] = vendor_gemm(torch, stream, a_d, w_d, b_d, o_d, m, n_rep, flops)
     if w is not None:
         out["producer_loop"] = producer_leg(F, torch, dev, stream, w, lm, trie, a_d, w_d, b_d, o_d, K)
     del a_d, w_d, b_d, o_d
+    return out
+
+
+def vendor_gemm(torch, stream, a_d, w_d, b_d, o_d, m, n_rep, flops):
+    """The same product from the vendor GEMM library (hipBLASLt through torch,
+    fp32 output) on the same inputs, for context: with the bias
+    (torch.addmm, the same work as joint_project) and without it (torch.mm,
+    less work), each with its largest difference from joint_project's output."""
+    a = a_d[:m].view(torch.bfloat16)
+    wt = w_d.view(torch.bfloat16).t()
+    forms = {"addmm_with_bias": lambda: torch.addmm(b_d, a, wt, out_dtype=torch.float32),
+             "mm_without_bias": lambda: torch.mm(a, wt, out_dtype=torch.float32)}
+    out = {"library": "hipBLASLt (through torch, out_dtype float32)"}
+    with torch.cuda.stream(stream):
+        for name, fn in forms.items():
+            for _ in range(3):
+                y = fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(n_rep):
+                y = fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / n_rep
+            ref = o_d[:m] if name == "addmm_with_bias" else o_d[:m] - b_d
+            out[name] = {"ms_per_launch": ms, "tflops": flops / (ms / 1e3) / 1e12,
+                         "max_abs_diff_vs_joint_project": float((y - ref).abs().max())}
+            del y, ref
     return out
 
 
