@@ -1,0 +1,168 @@
+"""GPU parity over seeded random configurations of the whole decode.
+
+Each case draws:
+- a vocabulary size around the widths the kernel is tiled by (the 4-token
+  lane strip, the 64-, 256- and 1024-lane workgroups);
+- n-gram orders 2..6, with one LM or two (two need V <= 4096);
+- the blank id (0 or another token);
+- a phrase list with or without completion bonuses, an empty list, or no
+  phrase tree;
+- k up to 8 candidates per hypothesis (1 in a greedy decode and in the
+  acoustic-argmax blank mode), and a greedy or beam decode with B up to 32,
+  with or without recombination;
+- random initial LM and phrase states, and random initial beam scores with
+  some slots dead.
+
+The fused score of Eq. (1) (Sec. III-C) is checked on one step from random
+states: full fused rows within 1e-5 of the oracle's fp64 values, with
+bit-exact top-k tokens and next states.
+
+A multi-frame decode (the frame loop and beam merge of Sec. IV-A) is then run
+in one call and compared with the oracle:
+- greedy decodes must equal the oracle's free-running decode token for token;
+- beam decodes are replayed by the oracle with the decisions taken on the GPU,
+  which must agree with its own except near ties (fp64 totals within 1e-4);
+- final states must be bit-exact and final scores within T x 1e-5.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_14991_amd as F
+from workloads import Phrases, tiny_random_lm, tiny_random_phrases
+
+pytestmark = pytest.mark.gpu
+
+SCORE_TOL = 1e-5
+TIE_TOL = 1e-4
+VOCABS = [2, 3, 5, 17, 63, 64, 65, 130, 255, 256, 257, 1000, 1023, 1024, 1025, 2047, 2049, 3000, 4096, 4097,
+          6000, 8190]
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def random_states(lm, n, rng):
+    """n valid LM state ids drawn over every order of context (plus <s>)."""
+    V = lm.vocab
+    ids = [V] + [int(t) for t in lm.tokens[0][:, 0] if t != V + 1 and t != lm.blank]
+    off = V + 2
+    for k in range(2, lm.order):
+        nk = lm.tokens[k - 1].shape[0]
+        ids += [off + i for i in range(nk) if lm.tokens[k - 1][i, -1] != V + 1]
+        off += nk
+    return rng.choice(np.array(ids, dtype=np.int64), size=n).astype(np.int32)
+
+
+class Case:
+    def __init__(self, seed):
+        rng = np.random.default_rng(7000 + seed)
+        self.rng = rng
+        V = int(rng.choice(VOCABS))
+        self.V = V
+        self.blank = 0 if V < 4 or rng.random() < 0.7 else int(rng.integers(1, V))
+        n_lm = 2 if (V <= 4096 and rng.random() < 0.3) else 1
+        n_max = 6  # the generator packs an n-gram into 63 bits: (V + 2)^N < 2^63
+        while (V + 2) ** n_max >= 2 ** 63:
+            n_max -= 1
+        self.lms = [tiny_random_lm(rng, V, int(rng.integers(2, n_max + 1)), n_sent=int(rng.integers(20, 400)),
+                                   blank=self.blank) for _ in range(n_lm)]
+        r = rng.random()
+        if r < 0.15:
+            self.ph = None
+        elif r < 0.25:
+            self.ph = Phrases(tokens=np.zeros(0, np.int32), offsets=np.zeros(1, np.int64))
+        else:
+            self.ph = tiny_random_phrases(rng, V, n=int(rng.integers(1, 40)), max_len=5, blank=self.blank,
+                                          alphabet=min(V - 1, int(rng.integers(2, 12))),
+                                          with_completion=bool(rng.random() < 0.5))
+        self.B = int(rng.choice([1, 1, 2, 3, 4, 4, 5, 8, 16, 32]))
+        if self.B == 1 and rng.random() < 0.4:
+            self.mode, self.k = F.FUSION_BLANK_AM, 1
+        else:
+            self.mode, self.k = F.FUSION_BLANK_COMPETE, int(rng.integers(1, min(8, V) + 1))
+        self.recombine = self.B > 1 and bool(rng.random() < 0.3)
+        self.S = int(rng.integers(1, 6))
+        self.T = int(rng.integers(2, 9))
+        self.alphas = [float(a) for a in rng.uniform(0.1, 1.2, n_lm)]
+        self.beta = float(rng.uniform(0.0, 1.5))
+        self.scale = float(rng.choice([0.5, 2.0, 4.0]))
+        self.bias = float(rng.uniform(0.0, 3.0))
+        self.glms = [F.ngram_load_arrays(m) for m in self.lms]
+        self.olms = [oracle.OracleLM(m) for m in self.lms]
+        self.gtr = None if self.ph is None else F.boost_build_phrases(V, self.blank, self.ph)
+        self.otr = None if self.ph is None else oracle.OracleTrie(V, self.blank, self.ph)
+        self.n_nodes = 1 if self.otr is None else self.otr.n_nodes
+
+    def __str__(self):
+        return (f"V={self.V} blank={self.blank} orders={[m.order for m in self.lms]} "
+                f"phrases={'none' if self.ph is None else self.ph.offsets.size - 1} B={self.B} k={self.k} "
+                f"mode={self.mode} recombine={self.recombine} S={self.S} T={self.T}")
+
+    def logits(self, *shape):
+        x = self.rng.standard_normal(shape) * self.scale
+        x[..., self.blank] += self.bias
+        return x.astype(np.float32)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_configuration(seed):
+    c = Case(seed)
+    print(f"case {seed}: {c}", flush=True)
+    rng, V, n_lm = c.rng, c.V, len(c.lms)
+
+    # one step from random states: fused rows, top-k and next states
+    H = 37
+    x = c.logits(H, V)
+    ls = np.stack([random_states(m, H, rng) for m in c.lms])
+    bs = rng.integers(0, c.n_nodes, size=H).astype(np.int32)
+    g = F.step_lms(c.glms, c.alphas, c.gtr, torch.from_numpy(x).to(dev()), torch.from_numpy(ls).to(dev()),
+                   torch.from_numpy(bs).to(dev()), c.beta, c.blank, c.k, c.mode, want_fused=True)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    r = oracle.step_lms(c.olms, c.alphas, c.otr, x, ls, bs, c.beta, c.blank, c.k, c.mode)
+    assert np.array_equal(g["tokens"].cpu().numpy(), r["tokens"]), "step tokens"
+    assert np.array_equal(g["next_lm"].cpu().numpy(), r["next_lm"]), "step next LM states"
+    if c.gtr is not None:
+        assert np.array_equal(g["next_boost"].cpu().numpy(), r["next_boost"]), "step next phrase states"
+    assert np.abs(g["fused"].cpu().numpy().astype(np.float64) - r["fused"]).max() <= SCORE_TOL
+    assert np.abs(g["scores"].cpu().numpy().astype(np.float64) - r["scores"]).max() <= SCORE_TOL
+
+    # a multi-frame decode in one call
+    S, B, T = c.S, c.B, c.T
+    H = S * B
+    k = 1 if B == 1 else c.k  # a greedy decode keeps one candidate
+    x = c.logits(T, H, V)
+    ls0 = np.stack([random_states(m, H, rng) for m in c.lms])
+    bs0 = rng.integers(0, c.n_nodes, size=H).astype(np.int32)
+    sc0 = None
+    if B > 1:
+        sc0 = -rng.uniform(0.0, 5.0, size=H)
+        sc0[rng.random(H) < 0.3] = -np.inf
+        sc0[::B] = np.where(np.isfinite(sc0[::B]), sc0[::B], 0.0)  # every stream keeps a live slot
+    ls = torch.from_numpy(ls0.copy()).to(dev())
+    bs = torch.from_numpy(bs0.copy()).to(dev())
+    sc = None if sc0 is None else torch.from_numpy(sc0.copy()).to(dev())
+    out = F.run_lms(c.glms, c.alphas, c.gtr, torch.from_numpy(x).to(dev()), S, B, k, c.beta, c.blank, c.mode,
+                    ls, bs, sc, recombine=c.recombine)
+    torch.cuda.synchronize()
+    assert F.fusion_device_status() == 0
+    if B == 1:
+        r = oracle.run_lms(c.olms, c.alphas, c.otr, x, S, 1, k, c.beta, c.blank, c.mode, ls0, bs0, threads=8)
+        assert np.array_equal(out["tokens"].cpu().numpy(), r["tokens"]), "greedy tokens"
+    else:
+        r = oracle.run_lms(c.olms, c.alphas, c.otr, x, S, B, k, c.beta, c.blank, c.mode, ls0, bs0, sc0,
+                           forced_tokens=out["tokens"].cpu().numpy(), forced_parents=out["parents"].cpu().numpy(),
+                           tol=TIE_TOL, threads=8, recombine=c.recombine)
+        bad = np.nonzero(r["mismatch_at"] >= 0)[0]
+        assert bad.size == 0, f"streams {bad[:8]} disagree beyond near ties (frames {r['mismatch_at'][bad[:8]]})"
+        got = sc.cpu().numpy()
+        fin = np.isfinite(r["hyp_score"])
+        assert np.array_equal(np.isfinite(got), fin)
+        assert np.abs(got[fin] - r["hyp_score"][fin]).max() <= T * SCORE_TOL
+    assert np.array_equal(ls.cpu().numpy().reshape(n_lm, H), np.asarray(r["lm_state"]).reshape(n_lm, H))
+    if c.gtr is not None:
+        assert np.array_equal(bs.cpu().numpy(), r["boost_state"])
