@@ -104,8 +104,10 @@ __device__ __forceinline__ unsigned long long mix64(unsigned long long z) {
   z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
   return z ^ (z >> 31);
 }
-// log(exp(a) + exp(b)) in fp64
-__device__ __forceinline__ double log_add(double a, double b) {
+// log(exp(a) + exp(b)) in fp64.  Not inlined: the merges that call it are rare,
+// and inlined, the constants of its exp and log1p would stay in vector
+// registers across the whole frame loop of the recombining kernel
+__device__ __attribute__((noinline)) double log_add(double a, double b) {
   const double m = a > b ? a : b, d = a > b ? b - a : a - b;
   return m + log1p(exp(d));
 }
@@ -1086,7 +1088,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       // candidate j ends in lane j
       int ck = INT_MIN, cy = INT_MAX;
       bool picked = false;
-      if constexpr (kSlots == 1 && KM > 1 && !RC) {  // (no registers to spare with recombination)
+      if constexpr (kSlots == 1 && KM > 1) {
         // at most 16 listed entries (the usual case after the wave-level
         // narrowing): compact them into LDS, let each count the entries ahead
         // of it (key desc, then id asc) in registers, and place it by that rank
@@ -1312,42 +1314,73 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
           // recombination: candidates that reach the same history (equal hash)
           // merge into the first of them in candidate order, with the log-sum
           // of their totals folded in that order; the others leave the ranking
-#pragma unroll 1
-          for (int i = lane; i < nc; i += 64) {
-            double m = __longlong_as_double(0x7FF8000000000000ll);
-            const double ti = s_tot[i];
-            if (ti == ti) {
-              const unsigned long long hi = s_hh[i];
-              int first = -1;
-              double acc = 0.0;
-#pragma unroll 1
-              for (int j = 0; j < nc; ++j) {
-                const double tj = s_tot[j];
-                if (tj == tj && s_hh[j] == hi) {
-                  if (first < 0) {
-                    first = j;
-                    acc = tj;
-                  } else {
-                    acc = log_add(acc, tj);
-                  }
+          if (nc <= 64) {
+            // one candidate per lane, every other candidate's total and hash
+            // read from its lane (readlane), not from LDS
+            const double ti = lane < nc ? s_tot[lane] : __longlong_as_double(0x7FF8000000000000ll);
+            const unsigned long long hi = lane < nc ? s_hh[lane] : 0ull;
+            const long long tb = __double_as_longlong(ti);
+            int first = -1;
+            double acc = 0.0;
+            for (int j = 0; j < nc; ++j) {
+              const double tj = __longlong_as_double(
+                  ((long long)(unsigned)__builtin_amdgcn_readlane((int)(tb >> 32), j) << 32) |
+                  (long long)(unsigned)__builtin_amdgcn_readlane((int)tb, j));
+              const unsigned long long hj =
+                  ((unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)(hi >> 32), j) << 32) |
+                  (unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)hi, j);
+              if (ti == ti && tj == tj && hj == hi) {
+                if (first < 0) {
+                  first = j;
+                  acc = tj;
+                } else {
+                  acc = log_add(acc, tj);
                 }
               }
-              if (first == i) m = acc;
             }
-            s_mt[i] = m;
-          }
-          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-          __builtin_amdgcn_wave_barrier();
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+            // every lane has read its own entry before any lane writes
+            if (lane < nc) s_tot[lane] = (ti == ti && first == lane) ? acc : __longlong_as_double(0x7FF8000000000000ll);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+          } else {
 #pragma unroll 1
-          for (int i = lane; i < nc; i += 64) s_tot[i] = s_mt[i];
-          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-          __builtin_amdgcn_wave_barrier();
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+            for (int i = lane; i < nc; i += 64) {
+              double m = __longlong_as_double(0x7FF8000000000000ll);
+              const double ti = s_tot[i];
+              if (ti == ti) {
+                const unsigned long long hi = s_hh[i];
+                int first = -1;
+                double acc = 0.0;
+#pragma unroll 1
+                for (int j = 0; j < nc; ++j) {
+                  const double tj = s_tot[j];
+                  if (tj == tj && s_hh[j] == hi) {
+                    if (first < 0) {
+                      first = j;
+                      acc = tj;
+                    } else {
+                      acc = log_add(acc, tj);
+                    }
+                  }
+                }
+                if (first == i) m = acc;
+              }
+              s_mt[i] = m;
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+#pragma unroll 1
+            for (int i = lane; i < nc; i += 64) s_tot[i] = s_mt[i];
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+          }
         }
         int wi = -1;
         bool ranked = false;
-        if (!RC && nc <= 16) {  // (the recombining variant has no registers to spare)
+        if (nc <= 16) {
           // up to 16 candidates (B * k <= 16; entries nc..15 hold NaN): every
           // lane loads all totals at once (eight 16-byte reads) and counts
           // those ahead of its own in registers; equal totals need the
