@@ -484,8 +484,8 @@ def main():
         copy_probe(args.copy_probe)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
-              "(the fusion path shards by stream with no per-step exchange; see DESIGN.md)",
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the fusion path would shard by stream, with no exchange between GPUs per step)",
               file=sys.stderr)
         sys.exit(2)
 
