@@ -641,12 +641,10 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     // per LM: order m of the state, its id; backoffs, first arcs and arc counts of
     // levels 2..m.  The first LM's context row (level D >= 2 of the chain, row r)
     // replaces the levels up to D: only the arcs of the levels above D are fetched
-    // (lcnt 0 for the others).  Further LMs fetch the arcs of every level.  The
-    // algorithmic bytes of the LM rows are counted here, over every level
+    // (lcnt 0 for the others).  Further LMs fetch the arcs of every level
     int m[NL], sid[NL], total_arcs[NL], Dc = 0, crow = 0;
     float bo[NL][kMaxLevels];
     int lcnt[NL][kMaxLevels], lbeg[NL][kMaxLevels];
-    unsigned long long lm_bytes = 0;
 #pragma unroll
     for (int i = 0; i < NL; ++i) {
       m[i] = rp[i] ? (rec[i][0] >> 16) : 1;
@@ -669,9 +667,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
         lcnt[i][L] = (lv && L > Di) ? rec[i][rec_cnt_word(L)] : 0;
         lbeg[i][L] = lv ? rec[i][rec_beg_word(L)] : 0;
         total_arcs[i] += lcnt[i][L];
-        if (lv) lm_bytes += umin64(8ull * (unsigned long long)(unsigned)rec[i][rec_cnt_word(L)], 4ull * V) + 12ull;
       }
-      if (m[i] >= 2) lm_bytes += 8ull;
     }
     if (CTX && ok && Dc >= 2) load_row(lms[0].ctx_lm + (int64_t)crow * V, lmval + NL * Vp, V);
     // ---- hop 2: first arcs of levels 2..m (flattened) and first phrase transitions --
@@ -1046,13 +1042,42 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       }
     }
     if (p.traffic && act && g == 0) {
+      // the frame's algorithmic bytes: the logits row; per LM the level-1 row and,
+      // for every level of the state's chain, its arc list (at most a row) and
+      // 12 bytes of record, plus 8 for a chain of two or more levels; the phrase
+      // node and its delta list.  Recomputed here from the frame's sources, which
+      // the hypothesis state holds until the install, so that the decode keeps
+      // no value alive for a count that only the counting launch takes
+      // The table pointers are read here through an address of the argument block
+      // that the compiler cannot see through: read where the loop could hoist
+      // them, they would hold scalar registers across the whole frame loop
+      const __attribute__((address_space(4))) char *kb =
+          (const __attribute__((address_space(4))) char *)__builtin_amdgcn_kernarg_segment_ptr();
+      asm volatile("" : "+s"(kb));
+      const __attribute__((address_space(4))) Params &pk = *(const __attribute__((address_space(4))) Params *)kb;
       unsigned long long by = 4ull * V;
       if (ok) {
         const unsigned long long row = 4ull * V;
+        const int y = hs.y;
 #pragma unroll
-        for (int i = 0; i < NL; ++i) by += umin64(8ull * (unsigned long long)lms[i].cnt1[c1[i]], row);
-        by += lm_bytes;
-        if (p.has_trie) by += 16ull + 16ull * (unsigned long long)dcnt;
+        for (int i = 0; i < NL; ++i) {
+          const int rs = pk.lm[i].rec_stride;
+          by += umin64(8ull * (unsigned long long)pk.lm[i].cnt1[hs.c1[i]], row);
+          const int src = hs.lmsrc[i];
+          const int32_t *r = src < -1  ? pk.lm[i].ctx_rec + ((int64_t)(-src - 2) * V + y) * rs
+                             : src < 0 ? pk.lm[i].rec_dense + ((int64_t)hs.c1p[i] * V + y) * rs
+                             : src >= V + 2 ? pk.lm[i].rec + (int64_t)(src - V - 2) * rs
+                                            : nullptr;
+          const int mi = r ? (r[0] >> 16) : 1;
+          for (int L = 2; L < kMaxLevels; ++L)
+            if (L <= mi) by += umin64(8ull * (unsigned long long)(unsigned)r[rec_cnt_word(L)], row) + 12ull;
+          if (mi >= 2) by += 8ull;
+        }
+        if (pk.has_trie) {
+          const int q = hs.qsrc;
+          const int4 nd = q < 0 ? pk.tr.root_node[y] : pk.tr.node[q];
+          by += 16ull + 16ull * (unsigned long long)nd.z;
+        }
       }
       by += BEAM ? 8ull : 4ull;
       if (p.fused) by += 4ull * V;
