@@ -93,6 +93,17 @@ struct Params {
   float lam[FUSION_MAX_LMS], beta;
 };
 
+// The kernel's argument block (its one argument, a Params, at offset 0) through an
+// address the compiler cannot see through: a field read from it is read where it
+// is used.  For pointers that only rare paths of the frame loop need; read as
+// plain arguments, they are hoisted out of the loop and hold scalar registers
+// across it (pushing other values into spill slots)
+__device__ __forceinline__ const __attribute__((address_space(4))) Params &args_here() {
+  const __attribute__((address_space(4))) char *kb =
+      (const __attribute__((address_space(4))) char *)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(kb));
+  return *(const __attribute__((address_space(4))) Params *)kb;
+}
 __device__ __forceinline__ bool before(float ka, int ya, float kb, int yb) {
   return ka > kb || (ka == kb && ya < yb);
 }
@@ -804,7 +815,6 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
     const bool want_keys = ok && (!blank_only || p.fused);
     const bool compete = p.mode == FUSION_BLANK_COMPETE;
     const bool write_fused = p.fused != nullptr && ok;
-    const rsrc_t fr = row_rsrc(write_fused ? p.fused + rowoff : p.logits, write_fused ? V : 0);
     float kk[NC][4];
     bool cd[NC][4];  // token (c, j) of this lane is a candidate
     // which tokens compete this frame (uniform): blank in blank-only frames or
@@ -902,6 +912,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       // this lane's entry values back to the root's for the next frame (read above)
       if (ER) *reinterpret_cast<float4 *>(erow + y0) = make_float4(rE[c][0], rE[c][1], rE[c][2], rE[c][3]);
       if (write_fused && y0 < V) {
+        const rsrc_t fr = row_rsrc(args_here().fused + rowoff, V);
         if (AL) {
           row_store4(fr, make_float4(kk[c][0] - lse, kk[c][1] - lse, kk[c][2] - lse, kk[c][3] - lse), voff, c * W * 16);
         } else {
@@ -1048,13 +1059,7 @@ __global__ void __launch_bounds__(W) fusion_kernel(Params p) {
       // node and its delta list.  Recomputed here from the frame's sources, which
       // the hypothesis state holds until the install, so that the decode keeps
       // no value alive for a count that only the counting launch takes
-      // The table pointers are read here through an address of the argument block
-      // that the compiler cannot see through: read where the loop could hoist
-      // them, they would hold scalar registers across the whole frame loop
-      const __attribute__((address_space(4))) char *kb =
-          (const __attribute__((address_space(4))) char *)__builtin_amdgcn_kernarg_segment_ptr();
-      asm volatile("" : "+s"(kb));
-      const __attribute__((address_space(4))) Params &pk = *(const __attribute__((address_space(4))) Params *)kb;
+      const __attribute__((address_space(4))) Params &pk = args_here();
       unsigned long long by = 4ull * V;
       if (ok) {
         const unsigned long long row = 4ull * V;
