@@ -108,7 +108,7 @@ class Case:
         return x.astype(np.float32)
 
 
-@pytest.mark.parametrize("seed", range(40))
+@pytest.mark.parametrize("seed", range(72))
 def test_random_configuration(seed):
     c = Case(seed)
     print(f"case {seed}: {c}", flush=True)
